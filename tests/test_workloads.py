@@ -1,0 +1,83 @@
+"""The synthetic workloads have the sizes the measurement plan states, and the
+KV content formula agrees between its device (torch) and host (numpy) forms."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+
+
+def test_shapes():
+    assert W.SHAPE_32L.bytes_per_token == 128 * 1024          # 8 GiB for a 64k-token prefix
+    assert W.SHAPE_80L.bytes_per_token == 320 * 1024
+    assert W.SHAPE_TINY.bytes_per_token == 1024
+    assert W.SHAPE_32L.seg_bytes == 32 * 1024
+    assert W.SHAPE_32L.slot_bytes == 32 * 1024 * 1024
+    assert W.SHAPE_80L.slot_bytes == 80 * 1024 * 1024
+
+
+def test_tiny():
+    w = W.tiny()
+    assert w.num_reqs == 8 and np.all(w.lengths == 256)
+    assert w.num_blocks == 128
+    for r in range(8):
+        assert np.array_equal(w.tokens[w.tok_off[r]:w.tok_off[r] + 128], w.prefix_streams[0][:128])
+    assert sorted(w.block_tables.ravel().tolist()) == list(range(128))
+    assert w.tokens.min() >= 0 and w.tokens.max() < 32000
+
+
+def test_l32_uniform():
+    w = W.l32_uniform()
+    assert w.num_reqs == 64 and w.tokens.size == 262144
+    assert w.num_blocks == 20480
+    assert len(w.prestage_chunks) == 64 and w.num_slots == 576
+    assert w.pool_bytes() == 40 * 2**30 and w.staged_bytes() == 18 * 2**30
+    bt = w.block_tables
+    assert bt.shape == (64, 256) and len(set(bt.ravel().tolist())) == 64 * 256
+
+
+def test_l80_long():
+    w = W.l80_long()
+    assert w.num_blocks == 18023 and w.num_slots == 1024
+    assert len(w.prestage_chunks) == 768
+
+
+def test_lognormal():
+    for ratio in (0.25, 0.5, 0.75):
+        w = W.l32_lognormal(ratio)
+        assert w.num_reqs == 256
+        assert w.lengths.min() >= 256 and w.lengths.max() <= 8192
+        assert 1700 < w.lengths.mean() < 2300
+        assert np.all(w.prefix_tokens % 256 == 0)
+
+
+def test_capacity():
+    full = W.l32_capacity(1.0, False)
+    assert full.num_blocks == 72090
+    assert np.all(full.prefix_tokens == 768)
+    u = full.notes["unique_prefixes"]
+    assert len(full.prestage_chunks) == 3 * u
+    half = W.l32_capacity(0.5, False)
+    quarter = W.l32_capacity(0.25, True)
+    assert len(half.prestage_chunks) <= round(1.5 * u) and len(half.prestage_chunks) % 3 == 0
+    assert len(quarter.prestage_chunks) <= round(0.75 * u) and quarter.staging_in_host
+
+
+@pytest.mark.parametrize("finite", [True, False])
+def test_fill_formula_device_form_matches_host_form(finite):
+    buf = torch.empty(1 << 16, dtype=torch.uint8)
+    W.fill_kv_(buf, 7, 3, finite=finite, chunk_words=1000)
+    ref = W.kv_bytes_np(7, 3, 0, buf.numel(), finite=finite)
+    assert np.array_equal(buf.numpy(), ref)
+    # an offset window recomputes the same bytes
+    assert np.array_equal(W.kv_bytes_np(7, 3, 4096, 512, finite), ref[4096:4096 + 512])
+    if finite:
+        halves = ref.view(np.uint16)
+        assert np.all((halves & 0x4000) == 0)
+
+
+def test_fill_formula_high_words():
+    # Words past 2^32 (buffers over 16 GiB) use the high half of the index.
+    a = W.kv_words_np(1, 1, (1 << 32) + 5, 4)
+    b = W.kv_words_np(1, 1, 5, 4)
+    assert not np.array_equal(a, b)
