@@ -1,0 +1,221 @@
+#!/usr/bin/env python3
+"""Benchmark of the KV staging hot path on one MI355X.
+
+One step is one pass of the whole path over the batch: prefix hash, lookup,
+one device-to-host copy of the lookup result, host job build and commitment
+decisions, one host-to-device copy of the jobs, the retrieve scatter, the
+store gather, and the index update (the chunks stored in the step are evicted
+again at its end, so every step does the same work).  Inputs (tokens, block
+tables, staging and pool contents) are resident in HBM before timing starts.
+
+Prints one JSON line: the whole-step payload rate in GB/s (bytes read plus
+bytes written by the scatter and the gather, divided by wall time per step),
+per-kernel rates measured with HIP events on the launch stream, the roofline
+of the dominant copy kernel against MI355X's 8 TB/s HBM peak, and the CPU
+oracle timed on a bounded sample of the same workload shape.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "paged-KV scatter/gather GB/s (% of HBM peak); prefix-hash Mtok/s"
+HBM_PEAK_GBS = 8000.0
+STG_TAG, POOL_TAG = 1, 1000
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def _src_digest() -> str:
+    h = hashlib.sha256()
+    for f in ("copy.hip", "internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_35065_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _load_traffic(kernel: str, workload: str):
+    """HBM bytes per launch measured by rocprofv3 counters, if a summary for
+    this kernel and workload exists and was taken from the current source."""
+    path = os.path.join(PROFILES, f"traffic_{kernel}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kvs = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.strip().split("=", 1)
+            kvs[k.strip()] = v.strip()
+    if kvs.get("source_digest") != _src_digest():
+        return None
+    try:
+        return float(kvs["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def _cpu_baseline(shape_name: str):
+    """The CPU oracle on a bounded sample with the benchmark's KV shape:
+    4 requests x 4096 tokens, 50% prefix from 2 shared prefixes (32 retrieve
+    and 32 store jobs, 2 GiB payload each way), one pass, single thread."""
+    import numpy as np
+    import workloads as W
+    from oracle.pipeline import OraclePath
+    shape = W.SHAPE_32L if shape_name == "l32" else W.SHAPE_80L
+    w = W._assemble("cpu-sample", shape, 2, [4096] * 4, [0, 1, 0, 1], [2048] * 4, 2,
+                    prestage=[(p, j) for p in range(2) for j in range(8)], num_slots=16 + 32, pool_factor=1.25)
+    o = OraclePath(w, kv_seed=2)
+    o.prestage()
+    t0 = time.perf_counter()
+    so = o.run_pass()
+    dt = time.perf_counter() - t0
+    moved = 2 * (len(so["retrieve"]) + len(so["store"])) * shape.slot_bytes
+    return {"value": round(moved / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": (f"one oracle pass (hash, lookup, job build, scatter, gather) over 4 requests x 4096 "
+                       f"tokens of the {shape.num_layers}-layer bf16 KV shape, 50% prefix from 2 shared prefixes: "
+                       f"{len(so['retrieve'])} retrieve + {len(so['store'])} store jobs, "
+                       f"{moved / 2**30:.1f} GiB moved in {dt:.2f} s, single-threaded C")}
+
+
+def _device_copy_gbs(torch, nbytes: int = 4 << 30, reps: int = 5) -> float:
+    """Plain device-to-device copy rate (read + write bytes / time): practical-peak context."""
+    a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    b.copy_(a)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    del a, b
+    torch.cuda.empty_cache()
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="l32-64x4096")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="only run a plain 4 GiB device copy 5 times (counter calibration) and exit")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the staging path shards by request with no exchange between "
+              "GPUs, so multi-GPU runs are not part of this benchmark (use --gpus 1).", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2609_35065_amd.pipeline import StagingPath
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    torch.cuda.set_device(0)
+    if args.calib_copy:
+        gbs = _device_copy_gbs(torch)
+        print(json.dumps({"calibration": "device copy", "bytes_per_dispatch": 4 << 30, "gbs_rw": round(gbs, 1)}))
+        return 0
+
+    w = W.make(args.workload)
+    print(f"[bench] workload {w.name}: {w.num_reqs} requests, pool {w.pool_bytes() / 2**30:.1f} GiB, "
+          f"staging {w.staged_bytes() / 2**30:.1f} GiB", file=sys.stderr, flush=True)
+    path = StagingPath(w)
+    path.fill(STG_TAG, POOL_TAG, w.seed)
+    path.prestage()
+    for _ in range(args.warmup):
+        path.run_pass(evict_stored=True)
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+
+    timers: dict = {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    stats = None
+    for _ in range(args.steps):
+        stats = path.run_pass(evict_stored=True, timers=timers)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    print(f"[bench] timed {args.steps} steps", file=sys.stderr, flush=True)
+
+    def avg_ms(name):
+        ev = timers.get(name, [])
+        return float(np.mean([a.elapsed_time(b) for a, b in ev])) if ev else 0.0
+
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    r_bytes = 2 * stats.retrieve_bytes          # read + write per step
+    s_bytes = 2 * stats.store_bytes
+    value = (r_bytes + s_bytes) / (ms_step * 1e-3) / 1e9
+    k_ms = {k: avg_ms(k) for k in ("hash", "lookup", "retrieve", "store")}
+    r_gbs = r_bytes / (k_ms["retrieve"] * 1e-3) / 1e9 if k_ms["retrieve"] else 0.0
+    s_gbs = s_bytes / (k_ms["store"] * 1e-3) / 1e9 if k_ms["store"] else 0.0
+    n_tok = int(w.tokens.size)
+    hash_mtok = n_tok / (k_ms["hash"] * 1e-3) / 1e6 if k_ms["hash"] else 0.0
+
+    dom = "retrieve" if k_ms["retrieve"] * 1 >= k_ms["store"] else "store"
+    dom_kernel = "kv_copy_retrieve" if dom == "retrieve" else "kv_copy_store"
+    achieved = r_gbs if dom == "retrieve" else s_gbs
+    traffic = _load_traffic(dom_kernel, args.workload)
+    # unique staged bytes a retrieve must read at least once + bytes written
+    uniq = len(set(int(q[0]) for q in path.last_retrieve)) * w.shape.slot_bytes
+    line = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": w.shape.num_layers, "kv_heads": w.shape.kv_heads,
+                   "head_dim": w.shape.head_dim, "block_size": w.shape.block_size,
+                   "chunk_tokens": w.shape.chunk_tokens, "requests": w.num_reqs, "tokens": n_tok,
+                   "pool_blocks": w.num_blocks, "staging_slots": w.num_slots,
+                   "retrieve_jobs": stats.num_retrieve, "store_jobs": stats.num_store},
+        "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic},
+        "kernels": {
+            "retrieve_scatter": {"ms": round(k_ms["retrieve"], 4), "GB/s": round(r_gbs, 1),
+                                 "frac_of_peak": round(r_gbs / HBM_PEAK_GBS, 4),
+                                 "payload_bytes_rw": r_bytes, "unique_min_bytes": uniq + stats.retrieve_bytes},
+            "store_gather": {"ms": round(k_ms["store"], 4), "GB/s": round(s_gbs, 1),
+                             "frac_of_peak": round(s_gbs / HBM_PEAK_GBS, 4), "payload_bytes_rw": s_bytes},
+            "hash_prefix": {"ms": round(k_ms["hash"], 4), "Mtok/s": round(hash_mtok, 1),
+                            "ns_per_chain_step": round(k_ms["hash"] * 1e6 / max(1, int(w.lengths.max()) // 16), 2)},
+            "lookup": {"ms": round(k_ms["lookup"], 4)},
+        },
+        "source_digest": _src_digest(),
+    }
+    del path
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    line["device_copy_GB/s"] = round(_device_copy_gbs(torch), 1)
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = _cpu_baseline("l80" if w.shape.num_layers == 80 else "l32")
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,256 @@
+/*
+ * tempokv.h -- C ABI of the TempoKV staging hot path on MI355X (gfx950).
+ *
+ * TempoKV (Park, Kim, Kim; "TempoKV: Timely Staging of LLM KV Caches for
+ * Memory-Semantic Flash") decides when to commit staging of reusable prefix
+ * KV.  Underneath its staging layer sit a prefix lookup and a fast-tier-to-GPU
+ * transfer that the paper reuses unchanged (Section 4, "Runtime and
+ * controller integration").  This library is that data path, MI355X-native:
+ *
+ *   kv_hash_prefix        chained 64-bit hash of token ids over 16-token blocks
+ *   kv_lookup             prefix match of chunk keys against a staged-chunk index
+ *   kv_build_jobs         host job build: hits -> retrieve jobs, misses -> store jobs
+ *   kv_retrieve_scatter   staged chunk [L,2,C,H,D] -> paged KV blocks (one launch)
+ *   kv_store_gather       paged KV blocks -> staged chunk (one launch)
+ *   kv_commit_should_stage  the TTU/TTR commitment rule of Section 3.2 (host)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Pointers named d_* are device-accessible (HBM, or mapped pinned host
+ *    memory for the staging buffer); h_* are host memory.  The caller owns
+ *    every buffer.  No call on the hot path allocates memory or keeps a
+ *    pointer after it returns.
+ *  - GPU calls enqueue work on `stream` (a hipStream_t; NULL = the default
+ *    stream) and return without synchronising.  Device faults surface at the
+ *    caller's next synchronisation.
+ *  - Return value: KV_OK (0) or a negative kv_status.  Argument errors are
+ *    detected before anything is enqueued; KV_EHIP reports a failed launch.
+ *  - Calls are reentrant; a kv_index must not be mutated concurrently.
+ */
+#ifndef TEMPOKV_H
+#define TEMPOKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KV_HASH_BLOCK_TOKENS 16   /* tokens per hash block */
+#define KV_MAX_LAYERS 128         /* layers one layout may name */
+
+typedef enum kv_status {
+    KV_OK = 0,
+    KV_EINVAL = -1,  /* null pointer, negative count, inconsistent shape or offsets */
+    KV_EALIGN = -2,  /* pointer or stride not 16-byte aligned */
+    KV_ERANGE = -3,  /* slot, request, chunk or block id out of range (kv_validate_jobs) */
+    KV_ENOSPC = -4,  /* no free staging slot for a miss, or the index is full */
+    KV_EHIP = -5,    /* a HIP runtime call or kernel launch failed */
+    KV_EDUP = -6     /* two jobs of one batch write the same block (scatter) or slot (gather) */
+} kv_status;
+
+/* Shapes and strides of the two KV layouts.
+ *   Staging slot s (one LMCache chunk of C tokens, Section 5 "Workload": only
+ *   complete 256-token chunks are retained) is [L][2][C][H][D] elements of
+ *   elem_bytes each, row-major, slot_bytes = L*2*C*H*D*elem_bytes apart.
+ *   Paged KV (vLLM): one device pointer per layer; the B-token block `blk` of
+ *   plane kv (0 = K, 1 = V) of layer l starts at
+ *       layer_ptrs[l] + kv*paged_kv_stride + blk*paged_block_stride
+ *   and holds [B][H][D] contiguous elements.  Per-layer [2][NB][B][H][D] is
+ *   kv_stride = NB*B*H*D*e, block_stride = B*H*D*e; [NB][2][B][H][D] is
+ *   kv_stride = B*H*D*e, block_stride = 2*B*H*D*e.
+ * Requirements: all counts > 0; num_layers <= KV_MAX_LAYERS; elem_bytes in
+ * {1, 2, 4} (the data is copied as opaque bits); chunk_tokens % block_size
+ * == 0; B*H*D*elem_bytes and both strides multiples of 16. */
+typedef struct kv_layout {
+    int32_t num_layers;        /* L */
+    int32_t kv_heads;          /* H */
+    int32_t head_dim;          /* D */
+    int32_t elem_bytes;        /* e */
+    int32_t block_size;        /* B, tokens per paged block */
+    int32_t chunk_tokens;      /* C, tokens per staged chunk */
+    int64_t num_blocks;        /* NB, paged blocks per layer */
+    int64_t num_slots;         /* S, staging slots */
+    int64_t paged_kv_stride;   /* bytes from the K plane to the V plane of a layer */
+    int64_t paged_block_stride;/* bytes between consecutive blocks of one plane */
+} kv_layout;
+
+/* One chunk transfer: staging slot <-> chunk `chunk` of request `req`, whose
+ * C/B paged blocks are block_tables[req*bt_stride + chunk*C/B + i]. 16 bytes;
+ * `reserved` must be 0. */
+typedef struct kv_job {
+    int32_t slot, req, chunk, reserved;
+} kv_job;
+
+/* ----------------------------------------------------------------------- */
+/* Prefix hash                                                              */
+/* ----------------------------------------------------------------------- */
+
+/* Chained block hashes of a ragged batch of token sequences.  The paper
+ * identifies reusable KV through LMCache's prefix lookup without defining it
+ * (Section 4); this library fixes the hash, over complete 16-token blocks
+ * (a trailing partial block has no hash, as the final incomplete chunk stays
+ * uncached, Section 5 "Workload").  With M the SplitMix64 finalizer and
+ * G = 0x9E3779B97F4A7C15, for request r and block b:
+ *     d_b = sum_{j<16} M(uint32(tok[16b+j]) + ((j+1) << 32))   (mod 2^64)
+ *     h_{-1} = seed,   h_b = M(h_{b-1} ^ d_b ^ G)
+ * d_tokens    int32 [d_tok_off[num_reqs]]  token ids, requests back to back
+ * d_tok_off   int64 [num_reqs+1]           token offsets (non-decreasing)
+ * d_blk_off   int64 [num_reqs+1]           output offsets; d_blk_off[r+1] -
+ *             d_blk_off[r] must equal floor(n_r/16) (not checked on device:
+ *             a request whose span differs writes min of the two counts)
+ * d_block_hash uint64 [d_blk_off[num_reqs]] output
+ * num_reqs == 0 enqueues nothing.  Errors: KV_EINVAL (null pointer, num_reqs
+ * < 0), KV_EHIP. */
+int kv_hash_prefix(const int32_t *d_tokens, const int64_t *d_tok_off, int32_t num_reqs,
+                   uint64_t seed, const int64_t *d_blk_off, uint64_t *d_block_hash, void *stream);
+
+/* ----------------------------------------------------------------------- */
+/* Staged-chunk index and lookup                                            */
+/* ----------------------------------------------------------------------- */
+
+/* Key -> staging slot map.  A KV object (Section 2.1) is one staged chunk,
+ * identified by its chunk key: the block hash at the chunk's last block, so a
+ * key names the whole token prefix that ends with that chunk.  The index is
+ * kept on the host (it is mutated by host policy) and mirrored to a device
+ * open-addressing table that kv_lookup probes.  Owns its host and device
+ * memory. */
+typedef struct kv_index kv_index;
+
+/* Create an index for up to max_entries live keys on the current device.
+ * Errors: KV_EINVAL (max_entries <= 0 or > 2^28, null out), KV_EHIP. */
+int kv_index_create(int64_t max_entries, kv_index **out);
+int kv_index_destroy(kv_index *idx);
+
+/* Insert or update n (key, slot) pairs given in host memory (slot >= 0), then
+ * enqueue the device-table update on `stream`; later work on that stream sees
+ * it.  A key already present takes the new slot.  Errors: KV_EINVAL,
+ * KV_ENOSPC (more than max_entries live keys; the pairs before the failing
+ * one stay inserted), KV_EHIP. */
+int kv_index_insert(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slots, int32_t n,
+                    void *stream);
+
+/* Remove n keys (absent keys are ignored), then enqueue the device-table
+ * update on `stream`. Errors: KV_EINVAL, KV_EHIP. */
+int kv_index_erase(kv_index *idx, const uint64_t *h_keys, int32_t n, void *stream);
+
+/* Number of live keys (host view). */
+int kv_index_size(const kv_index *idx, int64_t *out);
+
+/* Slot of one key on the host view, or -1.  For tests and host policy. */
+int kv_index_find(const kv_index *idx, uint64_t key, int32_t *slot_out);
+
+/* Prefix match (Section 2.1: once a prefix match is known the required
+ * objects and their order are known).  For request r with nb_r block hashes
+ * and bpc = blocks_per_chunk, chunk j < floor(nb_r/bpc) has key
+ * K[r][j] = d_block_hash[d_blk_off[r] + (j+1)*bpc - 1];
+ *   d_chunk_slot[d_chunk_off[r] + j] = slot of K[r][j], or -1 if absent
+ *   d_hit_chunks[r] = largest k such that every chunk j < k is present
+ * d_chunk_off int64 [num_reqs+1] must hold the prefix sums of
+ * floor(nb_r/bpc).  Errors: KV_EINVAL, KV_EHIP. */
+int kv_lookup(const kv_index *idx, const uint64_t *d_block_hash, const int64_t *d_blk_off,
+              int32_t num_reqs, int32_t blocks_per_chunk, const int64_t *d_chunk_off,
+              int32_t *d_chunk_slot, int32_t *d_hit_chunks, void *stream);
+
+/* ----------------------------------------------------------------------- */
+/* Host job build                                                           */
+/* ----------------------------------------------------------------------- */
+
+/* Turn a lookup result (copied to the host) into transfer jobs.
+ *   retrieve jobs: {chunk_slot, r, j} for every j < h_hit_chunks[r], in (r, j)
+ *     order -- the matched KV that retrieval moves to the GPU (Section 3.1);
+ *   store jobs: for chunks j >= h_hit_chunks[r] with chunk_slot == -1, in
+ *     (r, j) order, one job per distinct key (the first occurrence wins:
+ *     staging of one KV object is coalesced, Section 3.2 "Shared staging and
+ *     resource lifecycle"), with slots taken from h_free_slots in order.
+ *     h_store_keys[i] receives the key of store job i.
+ * h_retrieve and h_store must each hold h_chunk_off[num_reqs] jobs.
+ * Distinct missing keys beyond num_free get no job; *dropped counts them and
+ * the call returns KV_ENOSPC with the emitted jobs valid.  Errors: KV_EINVAL. */
+int kv_build_jobs(const int32_t *h_hit_chunks, const int32_t *h_chunk_slot,
+                  const uint64_t *h_block_hash, const int64_t *h_blk_off, const int64_t *h_chunk_off,
+                  int32_t num_reqs, int32_t blocks_per_chunk, const int32_t *h_free_slots,
+                  int32_t num_free, kv_job *h_retrieve, int32_t *num_retrieve, kv_job *h_store,
+                  uint64_t *h_store_keys, int32_t *num_store, int32_t *dropped);
+
+/* ----------------------------------------------------------------------- */
+/* Retrieve scatter and store gather                                        */
+/* ----------------------------------------------------------------------- */
+
+/* Retrieve (fast tier -> GPU, the transfer TTU counts down to, Section 3.1):
+ * for every job, layer l, plane kv and block i < C/B, copy the B-token
+ * segment at staging byte
+ *     slot*slot_bytes + ((l*2 + kv)*C + i*B)*H*D*e
+ * to paged block block_tables[req*bt_stride + chunk*C/B + i] of (l, kv).
+ * d_staging      device-accessible staging buffer [num_slots * slot_bytes]
+ * h_layer_ptrs   HOST array of num_layers device pointers (paged tensors)
+ * d_block_tables int32 [num_reqs][bt_stride] block ids
+ * d_jobs         kv_job [num_jobs] (device)
+ * Jobs whose slot, req or chunk is out of range, and segments whose block id
+ * is outside [0, num_blocks), are skipped: the kernel reads and writes only
+ * inside the described buffers.  Destinations must be disjoint within one
+ * call (kv_validate_jobs checks it); many jobs may read one slot.  One kernel
+ * launch per call; num_jobs == 0 enqueues nothing.
+ * Errors: KV_EINVAL, KV_EALIGN, KV_EHIP. */
+int kv_retrieve_scatter(const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
+                        const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
+                        const kv_job *d_jobs, int32_t num_jobs, void *stream);
+
+/* Store (retaining the KV of complete chunks, Section 5 "Workload"): the
+ * inverse walk, paged blocks of (req, chunk) -> staging slot.  Slots must be
+ * disjoint within one call.  Same arguments, checks and errors. */
+int kv_store_gather(const kv_layout *layout, void *d_staging, const void *const *h_layer_ptrs,
+                    const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
+                    const kv_job *d_jobs, int32_t num_jobs, void *stream);
+
+/* Host check of a job batch against copies of its tables: KV_ERANGE if any
+ * slot, request, chunk or (valid-job) block id is out of range or any
+ * reserved field is non-zero, KV_EDUP if two jobs write the same destination
+ * (scatter: paged block of a plane; gather, is_store != 0: staging slot),
+ * else KV_OK. */
+int kv_validate_jobs(const kv_layout *layout, const int32_t *h_block_tables, int32_t bt_stride,
+                     int32_t num_reqs, const kv_job *h_jobs, int32_t num_jobs, int is_store);
+
+/* ----------------------------------------------------------------------- */
+/* Commitment rule (host)                                                   */
+/* ----------------------------------------------------------------------- */
+
+typedef enum kv_commit_decision {
+    KV_DEFER = 0,    /* not eligible yet: laxity positive and no retrieval request */
+    KV_COMMIT = 1,   /* eligible and the footprint fits: request the commitment */
+    KV_BLOCKED = 2,  /* eligible, does not fit, no retrieval request: stays PLANNED */
+    KV_ORDINARY = 3  /* retrieval requested and protection unavailable: ordinary path */
+} kv_commit_decision;
+
+/* Section 3.2: laxity L = TTU - TTR; eligible iff L <= 0 (evaluated as
+ * ttu_s <= ttr_s, so infinite estimates behave) or retrieval_requested.  A
+ * commitment needs the claim's full footprint within the protected budget
+ * (claim_total_bytes <= budget_bytes) and its newly reserved bytes -- those
+ * not already covered by another commitment -- within the free protected
+ * capacity (claim_new_bytes <= free_protected_bytes).  Returns a
+ * kv_commit_decision, or KV_EINVAL for a NaN estimate or claim_new_bytes >
+ * claim_total_bytes.  Aging TTU by elapsed time is the caller's job. */
+int kv_commit_should_stage(double ttu_s, double ttr_s, uint64_t free_protected_bytes,
+                           uint64_t claim_new_bytes, uint64_t claim_total_bytes,
+                           uint64_t budget_bytes, int retrieval_requested);
+
+/* ----------------------------------------------------------------------- */
+/* Misc                                                                     */
+/* ----------------------------------------------------------------------- */
+
+/* Static description of a status code. */
+const char *kv_strerror(int status);
+
+/* Device address of mapped pinned host memory (hipHostMalloc'd), for staging
+ * buffers read zero-copy from host memory.  Errors: KV_EINVAL, KV_EHIP. */
+int kv_host_device_pointer(const void *h_ptr, void **d_ptr_out);
+
+/* Library version, e.g. "tempokv 0.1.0 gfx950". */
+const char *kv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TEMPOKV_H */

@@ -1,0 +1,315 @@
+"""Python binding of libtempokv (the C ABI declared in include/tempokv.h).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels or its native host code.  PyTorch supplies device memory and streams.
+The functions keep the C names; tensors are passed where the C call takes a
+device pointer, numpy arrays where it takes host memory.  A negative status
+raises ``KvError`` (``kv_build_jobs`` returns ``KV_ENOSPC`` instead, since its
+outputs stay valid).
+"""
+from __future__ import annotations
+
+import ctypes as ct
+import os
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtempokv.so")
+
+KV_OK, KV_EINVAL, KV_EALIGN, KV_ERANGE, KV_ENOSPC, KV_EHIP, KV_EDUP = 0, -1, -2, -3, -4, -5, -6
+KV_DEFER, KV_COMMIT, KV_BLOCKED, KV_ORDINARY = 0, 1, 2, 3
+KV_MAX_LAYERS = 128
+HASH_BLOCK_TOKENS = 16
+
+# every symbol include/tempokv.h declares
+EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
+           "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
+           "kv_store_gather", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
+           "kv_host_device_pointer", "kv_version"]
+
+
+class KvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {strerror(status)} ({status})")
+
+
+class KvLayout(ct.Structure):
+    _fields_ = [("num_layers", ct.c_int32), ("kv_heads", ct.c_int32), ("head_dim", ct.c_int32),
+                ("elem_bytes", ct.c_int32), ("block_size", ct.c_int32), ("chunk_tokens", ct.c_int32),
+                ("num_blocks", ct.c_int64), ("num_slots", ct.c_int64), ("paged_kv_stride", ct.c_int64),
+                ("paged_block_stride", ct.c_int64)]
+
+
+_lib: Optional[ct.CDLL] = None
+_vp, _i32, _i64, _u64, _dbl = ct.c_void_p, ct.c_int32, ct.c_int64, ct.c_uint64, ct.c_double
+
+
+def lib() -> ct.CDLL:
+    """Load libtempokv.so.  Raises if it has not been built: there is no
+    fallback implementation."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_35065_amd.build`")
+    # torch first: the library then binds to the HIP runtime torch already
+    # loaded (same soname), so torch's streams and allocations are its own.
+    import torch  # noqa: F401
+    L = ct.CDLL(LIB_PATH)
+    sig = {
+        "kv_hash_prefix": [_vp, _vp, _i32, _u64, _vp, _vp, _vp],
+        "kv_index_create": [_i64, ct.POINTER(_vp)],
+        "kv_index_destroy": [_vp],
+        "kv_index_insert": [_vp, _vp, _vp, _i32, _vp],
+        "kv_index_erase": [_vp, _vp, _i32, _vp],
+        "kv_index_size": [_vp, ct.POINTER(_i64)],
+        "kv_index_find": [_vp, _u64, ct.POINTER(_i32)],
+        "kv_lookup": [_vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp],
+        "kv_build_jobs": [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, ct.POINTER(_i32), _vp, _vp,
+                          ct.POINTER(_i32), ct.POINTER(_i32)],
+        "kv_retrieve_scatter": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
+        "kv_store_gather": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
+        "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
+        "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
+        "kv_strerror": [ct.c_int],
+        "kv_host_device_pointer": [_vp, ct.POINTER(_vp)],
+        "kv_version": [],
+    }
+    for name, args in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = ct.c_int
+    L.kv_strerror.restype = ct.c_char_p
+    L.kv_version.restype = ct.c_char_p
+    _lib = L
+    return L
+
+
+def strerror(status: int) -> str:
+    return lib().kv_strerror(status).decode()
+
+
+def kv_version() -> str:
+    return lib().kv_version().decode()
+
+
+def _check(rc: int, what: str) -> int:
+    if rc < 0:
+        raise KvError(rc, what)
+    return rc
+
+
+# ---------------------------------------------------------------------------
+# marshalling helpers
+# ---------------------------------------------------------------------------
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _dptr(t, dtype=None, what: str = "tensor") -> int:
+    """Device pointer of a contiguous CUDA (HIP) tensor, or an int address."""
+    if isinstance(t, int):
+        return t
+    import torch
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{what} must be {dtype}, got {t.dtype}")
+    return t.data_ptr()
+
+
+def _hptr(a: np.ndarray, dtype, what: str):
+    if not isinstance(a, np.ndarray) or a.dtype != dtype or not a.flags.c_contiguous:
+        raise ValueError(f"{what} must be a contiguous numpy {np.dtype(dtype)} array")
+    return a.ctypes.data
+
+
+def make_layout(num_layers: int, kv_heads: int, head_dim: int, elem_bytes: int, block_size: int,
+                chunk_tokens: int, num_blocks: int, num_slots: int, paged_kv_stride: int,
+                paged_block_stride: int) -> KvLayout:
+    return KvLayout(num_layers, kv_heads, head_dim, elem_bytes, block_size, chunk_tokens, num_blocks, num_slots,
+                    paged_kv_stride, paged_block_stride)
+
+
+# ---------------------------------------------------------------------------
+# the C calls
+# ---------------------------------------------------------------------------
+
+def kv_hash_prefix(d_tokens, d_tok_off, num_reqs: int, seed: int, d_blk_off, d_block_hash, stream=None) -> None:
+    import torch
+    _check(lib().kv_hash_prefix(_dptr(d_tokens, torch.int32, "tokens"), _dptr(d_tok_off, torch.int64, "tok_off"),
+                                num_reqs, seed & 0xFFFFFFFFFFFFFFFF, _dptr(d_blk_off, torch.int64, "blk_off"),
+                                _hash_ptr(d_block_hash), _stream(stream)), "kv_hash_prefix")
+
+
+def _hash_ptr(t) -> int:
+    """Block hashes are 64-bit words; an int64 (or uint64) tensor holds them."""
+    if isinstance(t, int):
+        return t
+    import torch
+    if t.dtype not in (torch.int64, getattr(torch, "uint64", torch.int64)):
+        raise ValueError(f"block_hash must be a 64-bit integer tensor, got {t.dtype}")
+    return _dptr(t, None, "block_hash")
+
+
+class KvIndex:
+    """Owner of a kv_index handle."""
+
+    def __init__(self, max_entries: int):
+        h = _vp()
+        _check(lib().kv_index_create(max_entries, ct.byref(h)), "kv_index_create")
+        self.handle = h
+        self.max_entries = max_entries
+
+    def insert(self, keys: np.ndarray, slots: np.ndarray, stream=None) -> None:
+        kv_index_insert(self, keys, slots, stream)
+
+    def erase(self, keys: np.ndarray, stream=None) -> None:
+        kv_index_erase(self, keys, stream)
+
+    def size(self) -> int:
+        return kv_index_size(self)
+
+    def find(self, key: int) -> int:
+        return kv_index_find(self, key)
+
+    def destroy(self) -> None:
+        if self.handle:
+            _check(lib().kv_index_destroy(self.handle), "kv_index_destroy")
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
+
+
+def kv_index_create(max_entries: int) -> KvIndex:
+    return KvIndex(max_entries)
+
+
+def kv_index_destroy(idx: KvIndex) -> None:
+    idx.destroy()
+
+
+def kv_index_insert(idx: KvIndex, keys: np.ndarray, slots: np.ndarray, stream=None) -> None:
+    keys = np.ascontiguousarray(keys, np.uint64)
+    slots = np.ascontiguousarray(slots, np.int32)
+    if keys.size != slots.size:
+        raise ValueError("keys and slots differ in length")
+    _check(lib().kv_index_insert(idx.handle, keys.ctypes.data, slots.ctypes.data, keys.size, _stream(stream)),
+           "kv_index_insert")
+
+
+def kv_index_erase(idx: KvIndex, keys: np.ndarray, stream=None) -> None:
+    keys = np.ascontiguousarray(keys, np.uint64)
+    _check(lib().kv_index_erase(idx.handle, keys.ctypes.data, keys.size, _stream(stream)), "kv_index_erase")
+
+
+def kv_index_size(idx: KvIndex) -> int:
+    n = _i64(0)
+    _check(lib().kv_index_size(idx.handle, ct.byref(n)), "kv_index_size")
+    return n.value
+
+
+def kv_index_find(idx: KvIndex, key: int) -> int:
+    s = _i32(0)
+    _check(lib().kv_index_find(idx.handle, key & 0xFFFFFFFFFFFFFFFF, ct.byref(s)), "kv_index_find")
+    return s.value
+
+
+def kv_lookup(idx: KvIndex, d_block_hash, d_blk_off, num_reqs: int, blocks_per_chunk: int, d_chunk_off,
+              d_chunk_slot, d_hit_chunks, stream=None) -> None:
+    import torch
+    _check(lib().kv_lookup(idx.handle, _hash_ptr(d_block_hash), _dptr(d_blk_off, torch.int64, "blk_off"),
+                           num_reqs, blocks_per_chunk, _dptr(d_chunk_off, torch.int64, "chunk_off"),
+                           _dptr(d_chunk_slot, torch.int32, "chunk_slot"),
+                           _dptr(d_hit_chunks, torch.int32, "hit_chunks"), _stream(stream)), "kv_lookup")
+
+
+def kv_build_jobs(hit_chunks: np.ndarray, chunk_slot: np.ndarray, block_hash: np.ndarray, blk_off: np.ndarray,
+                  chunk_off: np.ndarray, blocks_per_chunk: int, free_slots: np.ndarray):
+    """Returns (retrieve [n,4] int32, store [m,4] int32, store_keys [m] uint64, dropped, status)."""
+    R = blk_off.size - 1
+    nchunks = int(chunk_off[-1]) if R >= 0 and chunk_off.size else 0
+    hit = np.ascontiguousarray(hit_chunks, np.int32)
+    cs = np.ascontiguousarray(chunk_slot, np.int32)
+    bh = np.ascontiguousarray(block_hash, np.uint64)
+    bo = np.ascontiguousarray(blk_off, np.int64)
+    co = np.ascontiguousarray(chunk_off, np.int64)
+    fs = np.ascontiguousarray(free_slots, np.int32)
+    retr = np.zeros((max(nchunks, 1), 4), np.int32)
+    store = np.zeros((max(nchunks, 1), 4), np.int32)
+    keys = np.zeros(max(nchunks, 1), np.uint64)
+    nr, ns, nd = _i32(0), _i32(0), _i32(0)
+    rc = lib().kv_build_jobs(hit.ctypes.data, cs.ctypes.data, bh.ctypes.data, bo.ctypes.data, co.ctypes.data, R,
+                             blocks_per_chunk, fs.ctypes.data if fs.size else None, fs.size, retr.ctypes.data,
+                             ct.byref(nr), store.ctypes.data, keys.ctypes.data, ct.byref(ns), ct.byref(nd))
+    if rc < 0 and rc != KV_ENOSPC:
+        raise KvError(rc, "kv_build_jobs")
+    return retr[:nr.value].copy(), store[:ns.value].copy(), keys[:ns.value].copy(), nd.value, rc
+
+
+def _layer_array(layers: Sequence) -> ct.Array:
+    arr = (_vp * len(layers))()
+    for i, t in enumerate(layers):
+        arr[i] = _dptr(t, None, f"layer {i}")
+    return arr
+
+
+def kv_retrieve_scatter(layout: KvLayout, d_staging, layers: Sequence, d_block_tables, bt_stride: int,
+                        num_reqs: int, d_jobs, num_jobs: int, stream=None) -> None:
+    import torch
+    if len(layers) != layout.num_layers:
+        raise ValueError("one paged tensor per layer is required")
+    _check(lib().kv_retrieve_scatter(ct.byref(layout), _dptr(d_staging, None, "staging"), _layer_array(layers),
+                                     _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
+                                     _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
+                                     _stream(stream)), "kv_retrieve_scatter")
+
+
+def kv_store_gather(layout: KvLayout, d_staging, layers: Sequence, d_block_tables, bt_stride: int,
+                    num_reqs: int, d_jobs, num_jobs: int, stream=None) -> None:
+    import torch
+    if len(layers) != layout.num_layers:
+        raise ValueError("one paged tensor per layer is required")
+    _check(lib().kv_store_gather(ct.byref(layout), _dptr(d_staging, None, "staging"), _layer_array(layers),
+                                 _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
+                                 _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
+                                 _stream(stream)), "kv_store_gather")
+
+
+def kv_validate_jobs(layout: KvLayout, block_tables: np.ndarray, jobs: np.ndarray, is_store: bool) -> int:
+    """Returns KV_OK, KV_ERANGE or KV_EDUP (other errors raise)."""
+    bt = np.ascontiguousarray(block_tables, np.int32)
+    jb = np.ascontiguousarray(jobs, np.int32).reshape(-1, 4)
+    rc = lib().kv_validate_jobs(ct.byref(layout), bt.ctypes.data, bt.shape[1], bt.shape[0], jb.ctypes.data,
+                                jb.shape[0], 1 if is_store else 0)
+    if rc not in (KV_OK, KV_ERANGE, KV_EDUP):
+        raise KvError(rc, "kv_validate_jobs")
+    return rc
+
+
+def kv_commit_should_stage(ttu_s: float, ttr_s: float, free_protected_bytes: int, claim_new_bytes: int,
+                           claim_total_bytes: int, budget_bytes: int, retrieval_requested: bool) -> int:
+    """Returns a KV_DEFER/KV_COMMIT/KV_BLOCKED/KV_ORDINARY decision or KV_EINVAL."""
+    return lib().kv_commit_should_stage(ttu_s, ttr_s, free_protected_bytes, claim_new_bytes, claim_total_bytes,
+                                        budget_bytes, 1 if retrieval_requested else 0)
+
+
+def kv_host_device_pointer(host_ptr: int) -> int:
+    d = _vp()
+    _check(lib().kv_host_device_pointer(host_ptr, ct.byref(d)), "kv_host_device_pointer")
+    return d.value

@@ -1,0 +1,228 @@
+// api.hip -- the C ABI: argument checks, launch set-up, host job build, job
+// validation and the commitment rule.
+
+#include <math.h>
+#include <string.h>
+
+#include <unordered_set>
+#include <vector>
+
+#include "internal.h"
+
+namespace {
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Layout checks shared by the two copy directions.
+int check_layout(const kv_layout *lo) {
+    if (!lo) return KV_EINVAL;
+    if (lo->num_layers <= 0 || lo->num_layers > KV_MAX_LAYERS || lo->kv_heads <= 0 || lo->head_dim <= 0 ||
+        lo->block_size <= 0 || lo->chunk_tokens <= 0 || lo->num_blocks <= 0 || lo->num_slots <= 0)
+        return KV_EINVAL;
+    if (lo->elem_bytes != 1 && lo->elem_bytes != 2 && lo->elem_bytes != 4) return KV_EINVAL;
+    if (lo->chunk_tokens % lo->block_size != 0) return KV_EINVAL;
+    const int64_t seg = (int64_t)lo->block_size * lo->kv_heads * lo->head_dim * lo->elem_bytes;
+    if (seg > (int64_t(1) << 40)) return KV_EINVAL;
+    if (lo->paged_kv_stride <= 0 || lo->paged_block_stride <= 0) return KV_EINVAL;
+    if (lo->paged_block_stride < seg || lo->paged_kv_stride < seg) return KV_EINVAL;
+    if (seg % 16 != 0 || lo->paged_kv_stride % 16 != 0 || lo->paged_block_stride % 16 != 0) return KV_EALIGN;
+    // slot_bytes * num_slots must stay well inside int64
+    const int64_t slot = seg * (lo->chunk_tokens / lo->block_size) * 2 * lo->num_layers;
+    if (slot <= 0 || lo->num_slots > (int64_t(1) << 62) / slot) return KV_EINVAL;
+    return KV_OK;
+}
+
+int make_copy_params(tkv::CopyParams &p, const kv_layout *lo, const void *staging, const void *const *layers,
+                     const int32_t *bt, int32_t bt_stride, int32_t num_reqs, const kv_job *jobs,
+                     int32_t num_jobs) {
+    int rc = check_layout(lo);
+    if (rc != KV_OK) return rc;
+    if (num_jobs < 0 || num_reqs < 0 || bt_stride <= 0) return KV_EINVAL;
+    if (!staging || !layers || !bt || (num_jobs > 0 && !jobs)) return KV_EINVAL;
+    if (!aligned16(staging)) return KV_EALIGN;
+    memset(&p, 0, sizeof(p));
+    for (int l = 0; l < lo->num_layers; ++l) {
+        if (!layers[l]) return KV_EINVAL;
+        if (!aligned16(layers[l])) return KV_EALIGN;
+        p.layers[l] = (char *)layers[l];
+    }
+    const int32_t nseg = lo->chunk_tokens / lo->block_size;
+    p.staging = (char *)staging;
+    p.bt = bt;
+    p.jobs = jobs;
+    p.seg_bytes = (int64_t)lo->block_size * lo->kv_heads * lo->head_dim * lo->elem_bytes;
+    p.slot_bytes = p.seg_bytes * nseg * 2 * lo->num_layers;
+    p.kv_stride = lo->paged_kv_stride;
+    p.block_stride = lo->paged_block_stride;
+    p.num_blocks = lo->num_blocks;
+    p.num_slots = lo->num_slots;
+    p.L = lo->num_layers;
+    p.nseg = nseg;
+    p.bt_stride = bt_stride;
+    p.num_reqs = num_reqs;
+    p.num_jobs = num_jobs;
+    p.total_segs = (int64_t)num_jobs * lo->num_layers * 2 * nseg;
+    return KV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kv_hash_prefix(const int32_t *d_tokens, const int64_t *d_tok_off, int32_t num_reqs, uint64_t seed,
+                   const int64_t *d_blk_off, uint64_t *d_block_hash, void *stream) {
+    if (num_reqs < 0) return KV_EINVAL;
+    if (num_reqs == 0) return KV_OK;
+    if (!d_tokens || !d_tok_off || !d_blk_off || !d_block_hash) return KV_EINVAL;
+    return tkv::launch_hash(d_tokens, d_tok_off, num_reqs, seed, d_blk_off, d_block_hash, (hipStream_t)stream) ==
+                   hipSuccess
+               ? KV_OK
+               : KV_EHIP;
+}
+
+int kv_lookup(const kv_index *idx, const uint64_t *d_block_hash, const int64_t *d_blk_off, int32_t num_reqs,
+              int32_t blocks_per_chunk, const int64_t *d_chunk_off, int32_t *d_chunk_slot, int32_t *d_hit_chunks,
+              void *stream) {
+    if (!idx || num_reqs < 0 || blocks_per_chunk <= 0) return KV_EINVAL;
+    if (num_reqs == 0) return KV_OK;
+    if (!d_block_hash || !d_blk_off || !d_chunk_off || !d_chunk_slot || !d_hit_chunks) return KV_EINVAL;
+    int log2cap = 0;
+    const tkv::IndexEntry *table = tkv::index_device_table(idx, &log2cap);
+    return tkv::launch_lookup(table, log2cap, d_block_hash, d_blk_off, num_reqs, blocks_per_chunk, d_chunk_off,
+                              d_chunk_slot, d_hit_chunks, (hipStream_t)stream) == hipSuccess
+               ? KV_OK
+               : KV_EHIP;
+}
+
+int kv_retrieve_scatter(const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
+                        const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs, const kv_job *d_jobs,
+                        int32_t num_jobs, void *stream) {
+    tkv::CopyParams p;
+    const int rc = make_copy_params(p, layout, d_staging, (const void *const *)h_layer_ptrs, d_block_tables,
+                                    bt_stride, num_reqs, d_jobs, num_jobs);
+    if (rc != KV_OK) return rc;
+    return tkv::launch_copy(p, true, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
+}
+
+int kv_store_gather(const kv_layout *layout, void *d_staging, const void *const *h_layer_ptrs,
+                    const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs, const kv_job *d_jobs,
+                    int32_t num_jobs, void *stream) {
+    tkv::CopyParams p;
+    const int rc = make_copy_params(p, layout, d_staging, h_layer_ptrs, d_block_tables, bt_stride, num_reqs,
+                                    d_jobs, num_jobs);
+    if (rc != KV_OK) return rc;
+    return tkv::launch_copy(p, false, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
+}
+
+int kv_build_jobs(const int32_t *h_hit_chunks, const int32_t *h_chunk_slot, const uint64_t *h_block_hash,
+                  const int64_t *h_blk_off, const int64_t *h_chunk_off, int32_t num_reqs, int32_t blocks_per_chunk,
+                  const int32_t *h_free_slots, int32_t num_free, kv_job *h_retrieve, int32_t *num_retrieve,
+                  kv_job *h_store, uint64_t *h_store_keys, int32_t *num_store, int32_t *dropped) {
+    if (num_reqs < 0 || blocks_per_chunk <= 0 || num_free < 0) return KV_EINVAL;
+    if (!num_retrieve || !num_store || !dropped) return KV_EINVAL;
+    *num_retrieve = *num_store = *dropped = 0;
+    if (num_reqs == 0) return KV_OK;
+    if (!h_hit_chunks || !h_chunk_slot || !h_block_hash || !h_blk_off || !h_chunk_off || !h_retrieve ||
+        !h_store || !h_store_keys || (num_free > 0 && !h_free_slots))
+        return KV_EINVAL;
+    for (int32_t r = 0; r < num_reqs; ++r) {
+        const int64_t nb = h_blk_off[r + 1] - h_blk_off[r];
+        const int64_t nc = h_chunk_off[r + 1] - h_chunk_off[r];
+        if (nb < 0 || nc != nb / blocks_per_chunk || h_hit_chunks[r] < 0 || h_hit_chunks[r] > nc) return KV_EINVAL;
+    }
+    std::unordered_set<uint64_t> missing;   // distinct missing keys met so far
+    int32_t nr = 0, ns = 0, nd = 0;
+    for (int32_t r = 0; r < num_reqs; ++r) {
+        const int64_t c0 = h_chunk_off[r];
+        const int64_t nc = h_chunk_off[r + 1] - c0;
+        const int32_t hit = h_hit_chunks[r];
+        for (int32_t j = 0; j < hit; ++j) h_retrieve[nr++] = kv_job{h_chunk_slot[c0 + j], r, j, 0};
+        for (int64_t j = hit; j < nc; ++j) {
+            if (h_chunk_slot[c0 + j] >= 0) continue;
+            const uint64_t key = h_block_hash[h_blk_off[r] + (j + 1) * blocks_per_chunk - 1];
+            if (!missing.insert(key).second) continue;
+            if (ns >= num_free) {
+                ++nd;
+                continue;
+            }
+            h_store_keys[ns] = key;
+            h_store[ns] = kv_job{h_free_slots[ns], r, (int32_t)j, 0};
+            ++ns;
+        }
+    }
+    *num_retrieve = nr;
+    *num_store = ns;
+    *dropped = nd;
+    return nd > 0 ? KV_ENOSPC : KV_OK;
+}
+
+int kv_validate_jobs(const kv_layout *layout, const int32_t *h_block_tables, int32_t bt_stride, int32_t num_reqs,
+                     const kv_job *h_jobs, int32_t num_jobs, int is_store) {
+    int rc = check_layout(layout);
+    if (rc != KV_OK) return rc;
+    if (num_jobs < 0 || num_reqs < 0 || bt_stride <= 0) return KV_EINVAL;
+    if (num_jobs == 0) return KV_OK;
+    if (!h_block_tables || !h_jobs) return KV_EINVAL;
+    const int32_t nseg = layout->chunk_tokens / layout->block_size;
+    std::vector<uint8_t> seen(is_store ? (size_t)layout->num_slots : (size_t)layout->num_blocks, 0);
+    for (int32_t q = 0; q < num_jobs; ++q) {
+        const kv_job &jb = h_jobs[q];
+        if (jb.reserved != 0 || jb.slot < 0 || jb.slot >= layout->num_slots || jb.req < 0 || jb.req >= num_reqs ||
+            jb.chunk < 0 || (int64_t)(jb.chunk + 1) * nseg > bt_stride)
+            return KV_ERANGE;
+        for (int32_t i = 0; i < nseg; ++i) {
+            const int32_t blk = h_block_tables[(int64_t)jb.req * bt_stride + (int64_t)jb.chunk * nseg + i];
+            if (blk < 0 || blk >= layout->num_blocks) return KV_ERANGE;
+        }
+    }
+    for (int32_t q = 0; q < num_jobs; ++q) {
+        const kv_job &jb = h_jobs[q];
+        if (is_store) {
+            if (seen[jb.slot]++) return KV_EDUP;
+        } else {
+            for (int32_t i = 0; i < nseg; ++i) {
+                const int32_t blk = h_block_tables[(int64_t)jb.req * bt_stride + (int64_t)jb.chunk * nseg + i];
+                if (seen[blk]++) return KV_EDUP;
+            }
+        }
+    }
+    return KV_OK;
+}
+
+int kv_commit_should_stage(double ttu_s, double ttr_s, uint64_t free_protected_bytes, uint64_t claim_new_bytes,
+                           uint64_t claim_total_bytes, uint64_t budget_bytes, int retrieval_requested) {
+    if (isnan(ttu_s) || isnan(ttr_s) || claim_new_bytes > claim_total_bytes) return KV_EINVAL;
+    const bool eligible = ttu_s <= ttr_s || retrieval_requested != 0;
+    if (!eligible) return KV_DEFER;
+    const bool fits = claim_total_bytes <= budget_bytes && claim_new_bytes <= free_protected_bytes;
+    if (fits) return KV_COMMIT;
+    return retrieval_requested ? KV_ORDINARY : KV_BLOCKED;
+}
+
+const char *kv_strerror(int status) {
+    switch (status) {
+    case KV_OK: return "ok";
+    case KV_EINVAL: return "invalid argument";
+    case KV_EALIGN: return "pointer or stride not 16-byte aligned";
+    case KV_ERANGE: return "slot, request, chunk or block id out of range";
+    case KV_ENOSPC: return "no free staging slot or index full";
+    case KV_EHIP: return "HIP runtime error";
+    case KV_EDUP: return "duplicate destination within one batch";
+    default: return "unknown status";
+    }
+}
+
+int kv_host_device_pointer(const void *h_ptr, void **d_ptr_out) {
+    if (!h_ptr || !d_ptr_out) return KV_EINVAL;
+    void *d = nullptr;
+    if (hipHostGetDevicePointer(&d, const_cast<void *>(h_ptr), 0) != hipSuccess) {
+        (void)hipGetLastError();
+        return KV_EHIP;
+    }
+    *d_ptr_out = d;
+    return KV_OK;
+}
+
+const char *kv_version(void) { return "tempokv 0.1.0 gfx950"; }
+
+}  // extern "C"

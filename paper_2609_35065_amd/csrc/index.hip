@@ -1,0 +1,209 @@
+// index.hip -- the staged-chunk index: key -> staging slot.
+//
+// Host policy decides what is staged (job build allocates slots, eviction
+// frees them), so the authoritative table lives on the host; kv_lookup
+// probes a device mirror of it.  Both use the same open-addressing layout
+// (linear probing from a Fibonacci-hashed home position, tombstones for
+// erased keys), so a mutation is mirrored by uploading the table image.
+//
+// Uploads are stream-ordered: the table image is copied into one of two
+// pinned snapshot buffers and sent with hipMemcpyAsync on the caller's
+// stream, so a lookup enqueued after an insert on the same stream sees the
+// insert.  A snapshot buffer is reused only after the event recorded behind
+// its previous upload has completed.
+
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "internal.h"
+
+struct kv_index {
+    int device = 0;
+    int64_t max_entries = 0;
+    int log2cap = 0;
+    int64_t cap = 0;
+    int64_t live = 0;
+    int64_t tombs = 0;
+    std::vector<tkv::IndexEntry> host;
+    tkv::IndexEntry *dev = nullptr;
+    tkv::IndexEntry *snap[2] = {nullptr, nullptr};
+    hipEvent_t ev[2] = {nullptr, nullptr};
+    bool ev_used[2] = {false, false};
+    int next = 0;
+};
+
+namespace {
+
+using tkv::IndexEntry;
+using tkv::kEmpty;
+using tkv::kLive;
+using tkv::kTomb;
+
+// Position of `key`, or -1; *free_pos receives the first reusable position
+// met on the probe path (tombstone or empty), or -1 if none.
+int64_t probe(const kv_index *ix, uint64_t key, int64_t *free_pos) {
+    const uint64_t mask = (uint64_t)ix->cap - 1;
+    uint64_t pos = tkv::index_home(key, ix->log2cap);
+    int64_t first_free = -1;
+    for (int64_t n = 0; n < ix->cap; ++n) {
+        const IndexEntry &e = ix->host[pos];
+        if (e.state == kEmpty) {
+            if (first_free < 0) first_free = (int64_t)pos;
+            break;
+        }
+        if (e.state == kTomb) {
+            if (first_free < 0) first_free = (int64_t)pos;
+        } else if (e.key == key) {
+            if (free_pos) *free_pos = first_free;
+            return (int64_t)pos;
+        }
+        pos = (pos + 1) & mask;
+    }
+    if (free_pos) *free_pos = first_free;
+    return -1;
+}
+
+void rehash(kv_index *ix) {
+    std::vector<IndexEntry> old;
+    old.swap(ix->host);
+    ix->host.assign(ix->cap, IndexEntry{0, -1, kEmpty});
+    ix->tombs = 0;
+    const uint64_t mask = (uint64_t)ix->cap - 1;
+    for (const IndexEntry &e : old) {
+        if (e.state != kLive) continue;
+        uint64_t pos = tkv::index_home(e.key, ix->log2cap);
+        while (ix->host[pos].state != kEmpty) pos = (pos + 1) & mask;
+        ix->host[pos] = e;
+    }
+}
+
+int upload(kv_index *ix, hipStream_t stream) {
+    int prev = 0;
+    if (hipGetDevice(&prev) != hipSuccess) return KV_EHIP;
+    if (prev != ix->device && hipSetDevice(ix->device) != hipSuccess) return KV_EHIP;
+    int rc = KV_OK;
+    const int k = ix->next;
+    const size_t bytes = sizeof(IndexEntry) * (size_t)ix->cap;
+    if (ix->ev_used[k] && hipEventSynchronize(ix->ev[k]) != hipSuccess) rc = KV_EHIP;
+    if (rc == KV_OK) {
+        memcpy(ix->snap[k], ix->host.data(), bytes);
+        if (hipMemcpyAsync(ix->dev, ix->snap[k], bytes, hipMemcpyHostToDevice, stream) != hipSuccess ||
+            hipEventRecord(ix->ev[k], stream) != hipSuccess)
+            rc = KV_EHIP;
+        else
+            ix->ev_used[k] = true;
+    }
+    ix->next = k ^ 1;
+    if (prev != ix->device) (void)hipSetDevice(prev);
+    return rc;
+}
+
+void release(kv_index *ix) {
+    for (int k = 0; k < 2; ++k) {
+        if (ix->ev[k]) {
+            (void)hipEventSynchronize(ix->ev[k]);
+            (void)hipEventDestroy(ix->ev[k]);
+        }
+        if (ix->snap[k]) (void)hipHostFree(ix->snap[k]);
+    }
+    if (ix->dev) (void)hipFree(ix->dev);
+    delete ix;
+}
+
+}  // namespace
+
+namespace tkv {
+const IndexEntry *index_device_table(const kv_index *idx, int *log2cap) {
+    *log2cap = idx->log2cap;
+    return idx->dev;
+}
+}  // namespace tkv
+
+extern "C" {
+
+int kv_index_create(int64_t max_entries, kv_index **out) {
+    if (!out || max_entries <= 0 || max_entries > (int64_t(1) << 28)) return KV_EINVAL;
+    *out = nullptr;
+    kv_index *ix = new (std::nothrow) kv_index();
+    if (!ix) return KV_EINVAL;
+    ix->max_entries = max_entries;
+    ix->log2cap = 6;
+    while ((int64_t(1) << ix->log2cap) < 2 * max_entries) ++ix->log2cap;
+    ix->cap = int64_t(1) << ix->log2cap;
+    ix->host.assign(ix->cap, IndexEntry{0, -1, kEmpty});
+    const size_t bytes = sizeof(IndexEntry) * (size_t)ix->cap;
+    if (hipGetDevice(&ix->device) != hipSuccess || hipMalloc((void **)&ix->dev, bytes) != hipSuccess ||
+        hipMemset(ix->dev, 0, bytes) != hipSuccess ||
+        hipHostMalloc((void **)&ix->snap[0], bytes, hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc((void **)&ix->snap[1], bytes, hipHostMallocDefault) != hipSuccess ||
+        hipEventCreateWithFlags(&ix->ev[0], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ix->ev[1], hipEventDisableTiming) != hipSuccess ||
+        hipDeviceSynchronize() != hipSuccess) {
+        release(ix);
+        return KV_EHIP;
+    }
+    *out = ix;
+    return KV_OK;
+}
+
+int kv_index_destroy(kv_index *idx) {
+    if (!idx) return KV_EINVAL;
+    release(idx);
+    return KV_OK;
+}
+
+int kv_index_insert(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slots, int32_t n, void *stream) {
+    if (!idx || n < 0 || (n > 0 && (!h_keys || !h_slots))) return KV_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+        if (h_slots[i] < 0) return KV_EINVAL;
+    int rc = KV_OK;
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t free_pos = -1;
+        const int64_t at = probe(idx, h_keys[i], &free_pos);
+        if (at >= 0) {
+            idx->host[at].slot = h_slots[i];
+            continue;
+        }
+        if (idx->live >= idx->max_entries || free_pos < 0) {
+            rc = KV_ENOSPC;
+            break;
+        }
+        if (idx->host[free_pos].state == kTomb) --idx->tombs;
+        idx->host[free_pos] = IndexEntry{h_keys[i], h_slots[i], kLive};
+        ++idx->live;
+        if ((idx->live + idx->tombs) * 4 > idx->cap * 3) rehash(idx);
+    }
+    const int up = upload(idx, (hipStream_t)stream);
+    return rc != KV_OK ? rc : up;
+}
+
+int kv_index_erase(kv_index *idx, const uint64_t *h_keys, int32_t n, void *stream) {
+    if (!idx || n < 0 || (n > 0 && !h_keys)) return KV_EINVAL;
+    for (int32_t i = 0; i < n; ++i) {
+        const int64_t at = probe(idx, h_keys[i], nullptr);
+        if (at < 0) continue;
+        idx->host[at].state = kTomb;
+        idx->host[at].slot = -1;
+        --idx->live;
+        ++idx->tombs;
+    }
+    if ((idx->live + idx->tombs) * 4 > idx->cap * 3) rehash(idx);
+    return upload(idx, (hipStream_t)stream);
+}
+
+int kv_index_size(const kv_index *idx, int64_t *out) {
+    if (!idx || !out) return KV_EINVAL;
+    *out = idx->live;
+    return KV_OK;
+}
+
+int kv_index_find(const kv_index *idx, uint64_t key, int32_t *slot_out) {
+    if (!idx || !slot_out) return KV_EINVAL;
+    const int64_t at = probe(idx, key, nullptr);
+    *slot_out = at >= 0 ? idx->host[at].slot : -1;
+    return KV_OK;
+}
+
+}  // extern "C"

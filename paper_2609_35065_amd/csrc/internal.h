@@ -1,0 +1,62 @@
+// internal.h -- private declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tempokv.h"
+
+namespace tkv {
+
+// Device-table entry of the staged-chunk index: 16 bytes, read by one
+// dwordx4 load in the probe loop.
+struct alignas(16) IndexEntry {
+    uint64_t key;
+    int32_t slot;
+    int32_t state;   // kEmpty, kLive or kTomb
+};
+constexpr int32_t kEmpty = 0;
+constexpr int32_t kLive = 1;
+constexpr int32_t kTomb = 2;
+
+// Home position of a key in a table of 2^log2cap entries (Fibonacci
+// hashing: the high bits of key * 2^64/phi), so that any key set, including
+// small or sequential keys, spreads over the table.
+__host__ __device__ inline uint64_t index_home(uint64_t key, int log2cap) {
+    return (key * 0x9E3779B97F4A7C15ull) >> (64 - log2cap);
+}
+
+// Everything the copy kernels need, passed by value in the kernel-argument
+// segment so that the per-layer base pointers are read with scalar loads and
+// no device-side descriptor has to be allocated or uploaded.
+struct CopyParams {
+    char *staging;
+    char *layers[KV_MAX_LAYERS];
+    const int32_t *bt;
+    const kv_job *jobs;
+    int64_t slot_bytes;
+    int64_t seg_bytes;
+    int64_t kv_stride;
+    int64_t block_stride;
+    int64_t num_blocks;
+    int64_t num_slots;
+    int64_t total_segs;     // num_jobs * L * 2 * nseg
+    int32_t L;
+    int32_t nseg;           // C / B
+    int32_t bt_stride;
+    int32_t num_reqs;
+    int32_t num_jobs;
+};
+
+// Launchers (copy.hip, hash.hip).  Return hipSuccess or the launch error.
+hipError_t launch_copy(const CopyParams &p, bool retrieve, hipStream_t stream);
+hipError_t launch_hash(const int32_t *tokens, const int64_t *tok_off, int32_t num_reqs, uint64_t seed,
+                       const int64_t *blk_off, uint64_t *out, hipStream_t stream);
+hipError_t launch_lookup(const IndexEntry *table, int log2cap, const uint64_t *block_hash,
+                         const int64_t *blk_off, int32_t num_reqs, int32_t bpc, const int64_t *chunk_off,
+                         int32_t *chunk_slot, int32_t *hit_chunks, hipStream_t stream);
+
+// Device table of an index, for kv_lookup (index.cpp).
+const IndexEntry *index_device_table(const kv_index *idx, int *log2cap);
+
+}  // namespace tkv

@@ -1,0 +1,242 @@
+"""One pass of the staging hot path over a batch of requests, on one GPU.
+
+A pass is:  hash (kv_hash_prefix) -> lookup (kv_lookup) -> one device-to-host
+copy of the lookup result -> host job build (kv_build_jobs) and commitment
+decisions (kv_commit_should_stage) -> one host-to-device copy of the jobs ->
+retrieve scatter (kv_retrieve_scatter) -> store gather (kv_store_gather) ->
+index update (kv_index_insert; optionally kv_index_erase of what was just
+stored, which returns the batch to its starting state so that passes can be
+repeated).
+
+This module only sequences the C calls and owns the buffers they read and
+write; it computes nothing itself.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, kv_build_jobs, kv_commit_should_stage, kv_hash_prefix,
+               kv_host_device_pointer, kv_lookup, kv_retrieve_scatter, kv_store_gather, make_layout)
+
+
+@dataclass
+class PassStats:
+    num_retrieve: int = 0
+    num_store: int = 0
+    dropped: int = 0
+    retrieve_bytes: int = 0      # payload copied by the scatter (read = written)
+    store_bytes: int = 0
+    commits: int = 0
+    decisions: Dict[int, int] = field(default_factory=dict)
+
+
+class StagingPath:
+    """Device state of one workload: tokens, offsets, block tables, staging
+    buffer, per-layer paged KV tensors, the staged-chunk index and the host
+    free-slot list.
+
+    Parameters mirror the workload description (``workloads.Workload``): it
+    provides shapes, token ids, block tables and which chunks are staged at
+    the start.  KV contents are filled by the caller (see ``fill``)."""
+
+    def __init__(self, w, device: str = "cuda", hash_seed: int = 0, stream: Optional[torch.cuda.Stream] = None):
+        self.w = w
+        self.dev = torch.device(device)
+        self.hash_seed = hash_seed
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.dev)
+        s = w.shape
+        kv_stride, block_stride = w.strides()
+        self.layout: KvLayout = make_layout(s.num_layers, s.kv_heads, s.head_dim, s.elem_bytes, s.block_size,
+                                            s.chunk_tokens, w.num_blocks, w.num_slots, kv_stride, block_stride)
+        self.bpc = s.chunk_tokens // 16
+        d = self.dev
+        with torch.cuda.stream(self.stream):
+            self.staging_host = None
+            if w.staging_in_host:
+                self.staging_host = torch.empty(w.staged_bytes(), dtype=torch.uint8, pin_memory=True)
+                self.staging_ptr = kv_host_device_pointer(self.staging_host.data_ptr())
+                self.staging = None
+            else:
+                self.staging = torch.empty(w.staged_bytes(), dtype=torch.uint8, device=d)
+                self.staging_ptr = self.staging.data_ptr()
+            self.layers = [torch.empty(w.layer_bytes(), dtype=torch.uint8, device=d) for _ in range(s.num_layers)]
+        self.set_batch(w)
+        self.index = KvIndex(max(w.num_slots, 1))
+        self.free: List[int] = []
+        self.last_store_keys = np.zeros(0, np.uint64)
+        self.last_store_slots = np.zeros(0, np.int32)
+        self.last_retrieve = np.zeros((0, 4), np.int32)
+        self.last_store = np.zeros((0, 4), np.int32)
+
+    def set_batch(self, w) -> None:
+        """Load a new request batch (tokens, offsets, block tables) that uses
+        this path's KV shape, pool and staging buffer."""
+        assert w.shape == self.w.shape and w.num_blocks == self.w.num_blocks and w.num_slots == self.w.num_slots
+        self.batch = w
+        R = w.num_reqs
+        blk_off, chunk_off = w.offsets()
+        self.blk_off_h, self.chunk_off_h = blk_off, chunk_off
+        nblk, nch = int(blk_off[-1]), int(chunk_off[-1])
+        d = self.dev
+        with torch.cuda.stream(self.stream):
+            self.tokens = torch.from_numpy(w.tokens if w.tokens.size else np.zeros(1, np.int32)).to(d)
+            self.tok_off = torch.from_numpy(w.tok_off).to(d)
+            self.blk_off = torch.from_numpy(blk_off).to(d)
+            self.chunk_off = torch.from_numpy(chunk_off).to(d)
+            self.block_hash = torch.zeros(max(nblk, 1), dtype=torch.int64, device=d)
+            self.chunk_slot = torch.zeros(max(nch, 1), dtype=torch.int32, device=d)
+            self.hit = torch.zeros(max(R, 1), dtype=torch.int32, device=d)
+            self.bt = torch.from_numpy(np.ascontiguousarray(w.block_tables)).to(d)
+            self.d_retr = torch.zeros((max(nch, 1), 4), dtype=torch.int32, device=d)
+            self.d_store = torch.zeros((max(nch, 1), 4), dtype=torch.int32, device=d)
+        # pinned host mirrors for the one D2H and one H2D copy of a pass
+        self.h_block_hash = torch.zeros(max(nblk, 1), dtype=torch.int64, pin_memory=True)
+        self.h_chunk_slot = torch.zeros(max(nch, 1), dtype=torch.int32, pin_memory=True)
+        self.h_hit = torch.zeros(max(R, 1), dtype=torch.int32, pin_memory=True)
+        self.h_retr = torch.zeros((max(nch, 1), 4), dtype=torch.int32, pin_memory=True)
+        self.h_store = torch.zeros((max(nch, 1), 4), dtype=torch.int32, pin_memory=True)
+        self.stream.synchronize()
+
+    # ------------------------------------------------------------------
+    def staging_view(self) -> torch.Tensor:
+        return self.staging_host if self.staging is None else self.staging
+
+    def fill(self, staging_tag: int, pool_tag_base: int, seed: int, finite: bool = True) -> None:
+        """Fill staging and pool with the workload KV formula (input generation).
+        Layer l of the pool uses tag ``pool_tag_base + l``."""
+        from workloads import fill_kv_
+        with torch.cuda.stream(self.stream):
+            if self.staging is not None:
+                fill_kv_(self.staging, staging_tag, seed, finite)
+            else:
+                # host staging: fill device windows and copy them into the pinned buffer
+                n = self.staging_host.numel()
+                win = min(n, 1 << 30)
+                scratch = torch.empty(win, dtype=torch.uint8, device=self.dev)
+                for s0 in range(0, n, win):
+                    m = min(win, n - s0)
+                    fill_kv_(scratch[:m], staging_tag, seed, finite, byte_start=s0)
+                    self.staging_host[s0:s0 + m].copy_(scratch[:m])
+                del scratch
+            for l, t in enumerate(self.layers):
+                fill_kv_(t, pool_tag_base + l, seed, finite)
+        self.stream.synchronize()
+
+    def prestage(self) -> None:
+        """Index the chunks the workload says are staged at start: hash the
+        shared prefix streams with the library and insert their chunk keys
+        with slots 0..P-1 in workload order; the other slots are free."""
+        w = self.w
+        toks, off = w.prefix_stream_request()
+        P = len(w.prestage_chunks)
+        if P:
+            nb = np.diff(off) // 16
+            boff = np.zeros(off.size, np.int64)
+            np.cumsum(nb, out=boff[1:])
+            with torch.cuda.stream(self.stream):
+                dt = torch.from_numpy(toks if toks.size else np.zeros(1, np.int32)).to(self.dev)
+                doff = torch.from_numpy(off).to(self.dev)
+                dboff = torch.from_numpy(boff).to(self.dev)
+                dh = torch.zeros(max(int(boff[-1]), 1), dtype=torch.int64, device=self.dev)
+                kv_hash_prefix(dt, doff, off.size - 1, self.hash_seed, dboff, dh, self.stream)
+                h = dh.cpu().numpy().view(np.uint64)
+            keys = np.array([h[boff[p] + (j + 1) * self.bpc - 1] for p, j in w.prestage_chunks], np.uint64)
+            self.index.insert(keys, np.arange(P, dtype=np.int32), self.stream)
+        self.free = list(range(P, w.num_slots))
+        self.stream.synchronize()
+
+    # ------------------------------------------------------------------
+    def run_pass(self, evict_stored: bool = False, validate: bool = False, timers: Optional[dict] = None) -> PassStats:
+        """One pass of the hot path over the current batch.
+
+        ``timers``: optional dict; when given, a (start, end) pair of
+        torch.cuda.Event is appended under "hash", "lookup", "retrieve" and
+        "store" around each launch, recorded on this path's stream."""
+        w = self.batch
+        R = w.num_reqs
+        st = PassStats()
+        nblk, nch = int(self.blk_off_h[-1]), int(self.chunk_off_h[-1])
+        with torch.cuda.stream(self.stream):
+            e = self._ev(timers, "hash")
+            kv_hash_prefix(self.tokens, self.tok_off, R, self.hash_seed, self.blk_off, self.block_hash, self.stream)
+            self._ev_end(e)
+            e = self._ev(timers, "lookup")
+            kv_lookup(self.index, self.block_hash, self.blk_off, R, self.bpc, self.chunk_off, self.chunk_slot,
+                      self.hit, self.stream)
+            self._ev_end(e)
+            self.h_block_hash.copy_(self.block_hash, non_blocking=True)
+            self.h_chunk_slot.copy_(self.chunk_slot, non_blocking=True)
+            self.h_hit.copy_(self.hit, non_blocking=True)
+        self.stream.synchronize()
+        bh = self.h_block_hash.numpy()[:nblk].view(np.uint64)
+        cs = self.h_chunk_slot.numpy()[:nch]
+        hit = self.h_hit.numpy()[:R]
+        free = np.array(self.free, np.int32)
+        retr, store, skeys, dropped, rc = kv_build_jobs(hit, cs, bh, self.blk_off_h, self.chunk_off_h, self.bpc, free)
+        st.num_retrieve, st.num_store, st.dropped = len(retr), len(store), dropped
+        slot_bytes = w.shape.slot_bytes
+        st.retrieve_bytes = len(retr) * slot_bytes
+        st.store_bytes = len(store) * slot_bytes
+        # commitment decision per request claim: retrieval is requested now;
+        # the claim's matched footprint must fit the staged capacity
+        budget = self.w.num_slots * slot_bytes
+        for r in range(R):
+            if hit[r] > 0:
+                d = kv_commit_should_stage(0.0, 0.0, budget, 0, int(hit[r]) * slot_bytes, budget, True)
+                st.decisions[d] = st.decisions.get(d, 0) + 1
+                st.commits += int(d == KV_COMMIT)
+        if validate:
+            from . import kv_validate_jobs
+            assert kv_validate_jobs(self.layout, w.block_tables, retr, False) == 0 or len(retr) == 0
+            assert kv_validate_jobs(self.layout, w.block_tables, store, True) == 0 or len(store) == 0
+        nr, ns = len(retr), len(store)
+        with torch.cuda.stream(self.stream):
+            if nr:
+                self.h_retr.numpy()[:nr] = retr
+                self.d_retr[:nr].copy_(self.h_retr[:nr], non_blocking=True)
+            if ns:
+                self.h_store.numpy()[:ns] = store
+                self.d_store[:ns].copy_(self.h_store[:ns], non_blocking=True)
+            e = self._ev(timers, "retrieve")
+            kv_retrieve_scatter(self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_retr, nr,
+                                self.stream)
+            self._ev_end(e)
+            e = self._ev(timers, "store")
+            kv_store_gather(self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_store, ns,
+                            self.stream)
+            self._ev_end(e)
+            if ns:
+                self.index.insert(skeys, store[:, 0].copy(), self.stream)
+        used = set(int(x) for x in store[:, 0])
+        self.free = [s for s in self.free if s not in used]
+        self.last_store_keys, self.last_store_slots = skeys, store[:, 0].copy()
+        self.last_retrieve, self.last_store = retr, store
+        if evict_stored and ns:
+            self.evict_last()
+        return st
+
+    def _ev(self, timers, name):
+        if timers is None:
+            return None
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(self.stream)
+        timers.setdefault(name, []).append((a, b))
+        return b
+
+    def _ev_end(self, b) -> None:
+        if b is not None:
+            b.record(self.stream)
+
+    def evict_last(self) -> None:
+        """Erase the keys stored by the last pass and free their slots."""
+        if self.last_store_keys.size:
+            with torch.cuda.stream(self.stream):
+                self.index.erase(self.last_store_keys, self.stream)
+            self.free = sorted(self.free + [int(s) for s in self.last_store_slots])
+            self.last_store_keys = np.zeros(0, np.uint64)
+            self.last_store_slots = np.zeros(0, np.int32)
+

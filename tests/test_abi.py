@@ -1,0 +1,166 @@
+"""The C-ABI library without a GPU: it loads, exports every symbol the header
+declares, and its host-side logic (job build, job validation, commitment
+rule, argument checks) agrees with the oracle.  No call here reaches a
+kernel launch or a HIP allocation."""
+import ctypes as ct
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_35065_amd as kv
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "tempokv.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    declared = _declared()
+    assert len(declared) >= 15
+    assert sorted(kv.EXPORTS) == declared
+    L = ct.CDLL(kv.LIB_PATH)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_version_and_strerror():
+    assert "gfx950" in kv.kv_version()
+    for code in [0, -1, -2, -3, -4, -5, -6]:
+        assert kv.strerror(code) and kv.strerror(code) != "unknown status"
+    assert kv.strerror(-99) == "unknown status"
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_commit_rule_matches_oracle(seed):
+    rng = np.random.default_rng(seed)
+    vals = [-math.inf, -1.0, 0.0, 0.5, 1.0, 2.0, math.inf, math.nan]
+    for _ in range(300):
+        ttu, ttr = rng.choice(vals), rng.choice(vals)
+        free, new, total, budget = (int(x) for x in rng.integers(0, 10, 4))
+        req = bool(rng.integers(0, 2))
+        assert kv.kv_commit_should_stage(ttu, ttr, free, new, total, budget, req) == \
+            oracle.commit_should_stage(ttu, ttr, free, new, total, budget, req)
+
+
+def _lookup_case(seed):
+    rng = np.random.default_rng(seed)
+    C = int(rng.choice([16, 32, 64]))
+    bpc = C // 16
+    shared = rng.integers(0, 32000, 6 * C)
+    reqs = []
+    for _ in range(int(rng.integers(0, 9))):
+        k = int(rng.integers(0, 6)) * C
+        reqs.append(np.concatenate([shared[:k], rng.integers(0, 32000, int(rng.integers(0, 4 * C)))]).astype(np.int32))
+    if rng.random() < 0.3:
+        reqs += [r.copy() for r in reqs[:2]]
+    tok_off = np.zeros(len(reqs) + 1, np.int64)
+    np.cumsum([r.size for r in reqs], out=tok_off[1:])
+    toks = np.concatenate(reqs).astype(np.int32) if reqs else np.zeros(0, np.int32)
+    bh = oracle.hash_prefix(toks, tok_off)
+    blk_off = oracle.block_offsets(tok_off)
+    chunk_off = oracle.chunk_offsets(blk_off, bpc)
+    keys = oracle.chunk_keys(bh, blk_off, bpc)
+    st = shared.astype(np.int32)
+    sh = oracle.hash_prefix(st, np.array([0, st.size], np.int64))
+    index = {int(sh[(j + 1) * bpc - 1]): 50 + j for j in range(int(rng.integers(0, 6)))}
+    for k in keys[rng.random(keys.size) < 0.1]:
+        index.setdefault(int(k), 90)
+    cs, hit = oracle.lookup(index, bh, blk_off, bpc, chunk_off)
+    return bh, blk_off, chunk_off, bpc, cs, hit
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_build_jobs_matches_oracle(seed):
+    bh, blk_off, chunk_off, bpc, cs, hit = _lookup_case(seed)
+    rng = np.random.default_rng(seed + 100)
+    free = rng.permutation(200).astype(np.int32)[:int(rng.integers(0, 40))]
+    r1, s1, k1, d1 = oracle.build_jobs(hit, cs, bh, blk_off, chunk_off, bpc, free)
+    r2, s2, k2, d2, rc = kv.kv_build_jobs(hit, cs, bh, blk_off, chunk_off, bpc, free)
+    assert np.array_equal(r1, r2) and np.array_equal(s1, s2) and np.array_equal(k1, k2) and d1 == d2
+    assert rc == (kv.KV_ENOSPC if d2 else kv.KV_OK)
+
+
+def test_build_jobs_rejects_bad_offsets():
+    with pytest.raises(kv.KvError):
+        kv.kv_build_jobs(np.array([5], np.int32), np.zeros(1, np.int32), np.zeros(2, np.uint64),
+                         np.array([0, 2], np.int64), np.array([0, 1], np.int64), 2, np.zeros(0, np.int32))
+
+
+def _layout(**over):
+    d = dict(num_layers=2, kv_heads=2, head_dim=64, elem_bytes=2, block_size=16, chunk_tokens=64,
+             num_blocks=20, num_slots=4, paged_kv_stride=20 * 4096, paged_block_stride=4096)
+    d.update(over)
+    return kv.make_layout(**d)
+
+
+def test_validate_jobs():
+    lo = _layout()
+    bt = np.arange(20, dtype=np.int32)[::-1].reshape(2, 10).copy()
+    ok = np.array([[0, 0, 0, 0], [1, 1, 1, 0]], np.int32)
+    assert kv.kv_validate_jobs(lo, bt, ok, False) == kv.KV_OK
+    assert kv.kv_validate_jobs(lo, bt, ok, True) == kv.KV_OK
+    assert kv.kv_validate_jobs(lo, bt, np.array([[0, 0, 0, 0], [1, 0, 0, 0]], np.int32), False) == kv.KV_EDUP
+    assert kv.kv_validate_jobs(lo, bt, np.array([[2, 0, 0, 0], [2, 1, 0, 0]], np.int32), True) == kv.KV_EDUP
+    for bad in ([4, 0, 0, 0], [-1, 0, 0, 0], [0, 2, 0, 0], [0, 0, 2, 0], [0, 0, -1, 0], [0, 0, 0, 1]):
+        assert kv.kv_validate_jobs(lo, bt, np.array([bad], np.int32), False) == kv.KV_ERANGE
+    bt2 = bt.copy()
+    bt2[0, 2] = 20
+    assert kv.kv_validate_jobs(lo, bt2, ok, False) == kv.KV_ERANGE
+    bt2[0, 2] = -1
+    assert kv.kv_validate_jobs(lo, bt2, ok, True) == kv.KV_ERANGE
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(num_layers=0), kv.KV_EINVAL), (dict(num_layers=129), kv.KV_EINVAL), (dict(elem_bytes=3), kv.KV_EINVAL),
+    (dict(chunk_tokens=24), kv.KV_EINVAL), (dict(num_blocks=0), kv.KV_EINVAL), (dict(num_slots=0), kv.KV_EINVAL),
+    (dict(paged_block_stride=4096 + 8), kv.KV_EALIGN), (dict(paged_kv_stride=4104), kv.KV_EALIGN),
+    (dict(paged_block_stride=2048), kv.KV_EINVAL), (dict(kv_heads=1, head_dim=4, elem_bytes=1, block_size=2,
+                                                         chunk_tokens=4), kv.KV_EALIGN)])
+def test_copy_calls_reject_bad_layouts_before_any_launch(over, code):
+    lo = _layout(**over)
+    L = kv.lib()
+    layers = (ct.c_void_p * 128)(*([0x10000] * 128))
+    for f in (L.kv_retrieve_scatter, L.kv_store_gather):
+        assert f(ct.byref(lo), 0x10000, layers, 0x10000, 10, 2, 0x10000, 1, None) == code
+
+
+def test_copy_calls_reject_bad_pointers_before_any_launch():
+    lo = _layout()
+    L = kv.lib()
+    good = (ct.c_void_p * 2)(0x10000, 0x20000)
+    for f in (L.kv_retrieve_scatter, L.kv_store_gather):
+        assert f(ct.byref(lo), None, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), 0x10008, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EALIGN
+        assert f(ct.byref(lo), 0x10000, (ct.c_void_p * 2)(0x10000, 0x20004), 0x10000, 10, 2, 0x10000, 1,
+                 None) == kv.KV_EALIGN
+        assert f(ct.byref(lo), 0x10000, (ct.c_void_p * 2)(0x10000, None), 0x10000, 10, 2, 0x10000, 1,
+                 None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), 0x10000, good, None, 10, 2, 0x10000, 1, None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), 0x10000, good, 0x10000, 10, 2, None, 1, None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), 0x10000, good, 0x10000, 0, 2, 0x10000, 1, None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), 0x10000, good, 0x10000, 10, -1, 0x10000, 1, None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), 0x10000, good, 0x10000, 10, 2, 0x10000, -1, None) == kv.KV_EINVAL
+        assert f(None, 0x10000, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EINVAL
+        # zero jobs: valid, enqueues nothing
+        assert f(ct.byref(lo), 0x10000, good, 0x10000, 10, 2, None, 0, None) == kv.KV_OK
+
+
+def test_hash_and_lookup_argument_checks():
+    L = kv.lib()
+    assert L.kv_hash_prefix(None, None, 0, 0, None, None, None) == kv.KV_OK           # empty batch
+    assert L.kv_hash_prefix(None, 0x1000, 3, 0, 0x1000, 0x1000, None) == kv.KV_EINVAL
+    assert L.kv_hash_prefix(0x1000, 0x1000, -1, 0, 0x1000, 0x1000, None) == kv.KV_EINVAL
+    assert L.kv_lookup(None, 0x1000, 0x1000, 1, 1, 0x1000, 0x1000, 0x1000, None) == kv.KV_EINVAL
+    assert L.kv_index_create(0, ct.byref(ct.c_void_p())) == kv.KV_EINVAL
+    assert L.kv_index_create(10, None) == kv.KV_EINVAL
+    assert L.kv_index_destroy(None) == kv.KV_EINVAL
+    assert L.kv_index_insert(None, None, None, 0, None) == kv.KV_EINVAL
+    assert L.kv_host_device_pointer(None, ct.byref(ct.c_void_p())) == kv.KV_EINVAL

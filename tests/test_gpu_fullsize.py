@@ -1,0 +1,114 @@
+"""GPU parity at the full workload sizes, in the launch configuration the
+benchmark times.
+
+Buffers of 20-170 GiB cannot be held twice on the host, so:
+  * hash, lookup and the job lists are compared in full with the oracle;
+  * copies are checked on sampled segments: for a sampled paged block the
+    oracle says (one by one) which staged segment, if any, lands there, and
+    the expected bytes are recomputed from the input generator's formula; the
+    same for sampled staging segments written by the store gather.  Samples
+    cover every layer, both planes, the first and last jobs, and blocks that
+    no job touches (which must keep their original bytes)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from oracle.pipeline import OraclePath
+from paper_2609_35065_amd.pipeline import StagingPath
+
+pytestmark = pytest.mark.gpu
+
+STG_TAG, POOL_TAG = 1, 1000
+
+
+def _seg_view(w, layer_tensor, kv, blk):
+    seg = w.shape.seg_bytes
+    kvs, bs = w.strides()
+    off = kv * kvs + blk * bs
+    return layer_tensor[off:off + seg], off
+
+
+def check_full_size(name, n_samples=600, seed=0):
+    w = W.make(name)
+    print(f"[fullsize] {name}: {w.num_reqs} reqs, pool {w.pool_bytes() / 2**30:.1f} GiB, "
+          f"staging {w.staged_bytes() / 2**30:.1f} GiB", flush=True)
+    g = StagingPath(w)
+    g.fill(STG_TAG, POOL_TAG, w.seed)
+    g.prestage()
+    o = OraclePath(w, with_kv=False)
+    o.prestage()
+    sg = g.run_pass(validate=True)
+    so = o.run_pass()
+    torch.cuda.synchronize()
+    nblk, nch, R = int(g.blk_off_h[-1]), int(g.chunk_off_h[-1]), w.num_reqs
+    assert np.array_equal(g.h_block_hash.numpy()[:nblk].view(np.uint64), so["block_hash"])
+    assert np.array_equal(g.h_chunk_slot.numpy()[:nch], so["chunk_slot"])
+    assert np.array_equal(g.h_hit.numpy()[:R], so["hit"])
+    assert np.array_equal(g.last_retrieve, so["retrieve"])
+    assert np.array_equal(g.last_store, so["store"])
+    # the hit counts follow from the workload's construction
+    C = w.shape.chunk_tokens
+    resident = set(p for p, _ in w.prestage_chunks)
+    exp_hit = np.array([w.prefix_tokens[r] // C if w.prefix_id[r] in resident else 0 for r in range(R)])
+    assert np.array_equal(so["hit"], exp_hit)
+
+    rng = np.random.default_rng(seed)
+    L, seg = w.shape.num_layers, w.shape.seg_bytes
+    retr, store = so["retrieve"], so["store"]
+    # --- scatter: sampled destination blocks, touched and untouched
+    nseg = C // w.shape.block_size
+    touched = np.unique(np.concatenate([w.block_tables[q[1], q[2] * nseg:(q[2] + 1) * nseg] for q in retr])) \
+        if len(retr) else np.zeros(0, np.int32)
+    picks = []
+    if len(retr):
+        for q in (retr[0], retr[-1]):
+            for i in range(nseg):
+                picks.append((int(rng.integers(0, L)), int(rng.integers(0, 2)),
+                              int(w.block_tables[q[1], q[2] * nseg + i])))
+        for b in rng.choice(touched, min(n_samples, touched.size), replace=False):
+            picks.append((int(rng.integers(0, L)), int(rng.integers(0, 2)), int(b)))
+    for b in rng.integers(0, w.num_blocks, n_samples // 4):
+        picks.append((int(rng.integers(0, L)), int(rng.integers(0, 2)), int(b)))
+    n_touched = 0
+    for l, kvp, blk in picks:
+        got, off = _seg_view(w, g.layers[l], kvp, blk)
+        got = got.cpu().numpy()
+        src = oracle.scatter_source(o.layout, w.block_tables, retr, l, kvp, blk)
+        if src is None:
+            exp = W.kv_bytes_np(POOL_TAG + l, w.seed, off, seg)
+        else:
+            n_touched += 1
+            exp = W.kv_bytes_np(STG_TAG, w.seed, src, seg)
+        assert np.array_equal(got, exp), (name, "scatter", l, kvp, blk)
+    if len(retr):
+        assert n_touched > 0
+    # --- gather: sampled staging segments of the stored slots
+    if len(store):
+        slots = [int(store[0, 0]), int(store[-1, 0])] + [int(s) for s in rng.choice(store[:, 0], min(40, len(store)))]
+        stg = g.staging_view()
+        for s in slots:
+            for _ in range(8):
+                l, kvp, i = int(rng.integers(0, L)), int(rng.integers(0, 2)), int(rng.integers(0, nseg))
+                so_off = s * w.shape.slot_bytes + ((l * 2 + kvp) * nseg + i) * seg
+                got = stg[so_off:so_off + seg].cpu().numpy()
+                blk = oracle.gather_source(o.layout, w.block_tables, store, s, i)
+                assert blk is not None
+                _, poff = _seg_view(w, g.layers[l], kvp, blk)
+                exp = W.kv_bytes_np(POOL_TAG + l, w.seed, poff, seg)
+                assert np.array_equal(got, exp), (name, "gather", s, l, kvp, i)
+    del g
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return sg, so
+
+
+FULL = ["l32-64x4096", "l32-lognormal-p25", "l32-lognormal-p50", "l32-lognormal-p75", "l80-32x8192",
+        "l32-1024x1024-cap100-hbm", "l32-1024x1024-cap50-hbm", "l32-1024x1024-cap25-hbm",
+        "l32-1024x1024-cap25-host"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_full_size_sampled(name):
+    check_full_size(name)

@@ -1,0 +1,303 @@
+"""GPU parity: the HIP path against the CPU oracle, bit for bit.
+
+Every test runs the library through its C ABI (via the Python binding) and
+the oracle on the same seeded inputs, and compares outputs exactly: block
+hashes, lookup results, job lists, and every byte of the staging buffer and
+the paged pool.  Inputs come from the workload generator only."""
+import copy
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_35065_amd as kv
+import workloads as W
+from oracle.pipeline import OraclePath
+from paper_2609_35065_amd.pipeline import StagingPath
+
+pytestmark = pytest.mark.gpu
+
+STG_TAG, POOL_TAG = 1, 1000
+
+
+def _pair(w, kv_seed=None, finite=True, hash_seed=0):
+    kv_seed = w.seed if kv_seed is None else kv_seed
+    g = StagingPath(w, hash_seed=hash_seed)
+    g.fill(STG_TAG, POOL_TAG, kv_seed, finite)
+    g.prestage()
+    o = OraclePath(w, hash_seed=hash_seed, kv_seed=kv_seed, finite=finite, staging_tag=STG_TAG,
+                   pool_tag_base=POOL_TAG)
+    o.prestage()
+    return g, o
+
+
+def _compare_pass(g, o, sg, so, check_kv=True):
+    torch.cuda.synchronize()
+    nblk = int(g.blk_off_h[-1])
+    nch = int(g.chunk_off_h[-1])
+    R = g.batch.num_reqs
+    assert np.array_equal(g.h_block_hash.numpy()[:nblk].view(np.uint64), so["block_hash"])
+    assert np.array_equal(g.h_chunk_slot.numpy()[:nch], so["chunk_slot"])
+    assert np.array_equal(g.h_hit.numpy()[:R], so["hit"])
+    assert np.array_equal(g.last_retrieve, so["retrieve"])
+    assert np.array_equal(g.last_store, so["store"])
+    assert sg.dropped == so["dropped"]
+    if check_kv:
+        assert np.array_equal(g.staging_view().cpu().numpy(), o.staging), "staging differs"
+        for l in range(len(g.layers)):
+            assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l]), f"layer {l} differs"
+
+
+def _free(*objs):
+    for x in objs:
+        del x
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# tiny workload: store every chunk, then retrieve the hits
+# ---------------------------------------------------------------------------
+
+def test_tiny_store_all_then_retrieve_all():
+    w = W.tiny()
+    g, o = _pair(w)
+    sg, so = g.run_pass(validate=True), o.run_pass()
+    _compare_pass(g, o, sg, so)
+    assert sg.num_retrieve == 0 and sg.num_store == 18      # 4 chunks of request 0, 2 private x 7
+    # sentinel pool, fresh block tables, retrieve everything back
+    for t in g.layers:
+        t.fill_(0xA5)
+    for a in o.layers:
+        a[:] = 0xA5
+    w2 = copy.deepcopy(w)
+    W.repermute_block_tables(w2, 1)
+    g.set_batch(w2)
+    o.set_batch(w2)
+    sg, so = g.run_pass(validate=True), o.run_pass()
+    _compare_pass(g, o, sg, so)
+    assert sg.num_retrieve == 32 and sg.num_store == 0
+    assert all(np.all(so["hit"] == 4) for _ in [0])
+    # the pool is exactly the live blocks, so no sentinel block remains
+    for l in range(w.shape.num_layers):
+        segs = g.layers[l].cpu().numpy().reshape(2, w.num_blocks, -1)
+        assert not np.any(np.all(segs == 0xA5, axis=-1))
+
+
+def test_tiny_store_one_request_then_partial_hits():
+    w = W.tiny()
+    w0 = copy.deepcopy(w)
+    w0.tokens = w.tokens[:256].copy()
+    w0.tok_off = np.array([0, 256], np.int64)
+    w0.block_tables = w.block_tables[:1].copy()
+    g, o = _pair(w)
+    g.set_batch(w0)
+    o.set_batch(w0)
+    sg, so = g.run_pass(validate=True), o.run_pass()
+    _compare_pass(g, o, sg, so)
+    assert sg.num_store == 4
+    for t in g.layers:
+        t.fill_(0x5A)
+    for a in o.layers:
+        a[:] = 0x5A
+    g.set_batch(w)
+    o.set_batch(w)
+    sg, so = g.run_pass(validate=True), o.run_pass()
+    _compare_pass(g, o, sg, so)
+    assert list(so["hit"]) == [4] + [2] * 7
+    assert sg.num_retrieve == 18 and sg.num_store == 14
+    # blocks no retrieve job wrote keep the sentinel
+    written = set(int(b) for q in so["retrieve"] for b in
+                  w.block_tables[q[1], q[2] * 4:(q[2] + 1) * 4])
+    for l in range(w.shape.num_layers):
+        segs = g.layers[l].cpu().numpy().reshape(2, w.num_blocks, -1)
+        for blk in range(w.num_blocks):
+            assert np.all(segs[:, blk] == 0x5A) == (blk not in written)
+
+
+# ---------------------------------------------------------------------------
+# random small workloads over shapes and layouts
+# ---------------------------------------------------------------------------
+
+SHAPES = [W.KVShape(2, 2, 64, 2, 16, 64), W.KVShape(3, 1, 64, 2, 16, 16), W.KVShape(1, 8, 128, 2, 16, 256),
+          W.KVShape(2, 2, 128, 2, 32, 128), W.KVShape(2, 1, 64, 1, 32, 32), W.KVShape(1, 2, 64, 4, 16, 64),
+          W.KVShape(4, 8, 64, 2, 32, 512), W.KVShape(2, 1, 128, 2, 16, 16)]
+
+
+@pytest.mark.parametrize("layout", ["kv_first", "block_first"])
+@pytest.mark.parametrize("si", range(len(SHAPES)))
+def test_random_workloads(si, layout):
+    shape = SHAPES[si]
+    w = W.small_random(100 + si, shape, num_reqs=9, max_len=5 * shape.chunk_tokens + 37, paged_layout=layout)
+    g, o = _pair(w)
+    for p in range(3):       # stores, then hits on what was stored, then an evicting pass
+        evict = p == 2
+        sg, so = g.run_pass(validate=True, evict_stored=evict), o.run_pass(evict_stored=evict)
+        _compare_pass(g, o, sg, so)
+    _free(g, o)
+
+
+def test_raw_bit_patterns_nan_payloads():
+    shape = W.KVShape(2, 2, 64, 2, 16, 64)
+    w = W.small_random(7, shape, num_reqs=6, max_len=300)
+    g, o = _pair(w, finite=False)
+    sg, so = g.run_pass(validate=True), o.run_pass()
+    _compare_pass(g, o, sg, so)
+    sg, so = g.run_pass(validate=True), o.run_pass()
+    _compare_pass(g, o, sg, so)
+    halves = g.staging_view().cpu().numpy().view(np.uint16)
+    assert np.any((halves & 0x7C00) == 0x7C00)              # fp16 Inf/NaN patterns were moved too
+
+
+def test_slot_exhaustion_drops_misses():
+    shape = W.KVShape(1, 2, 64, 2, 16, 32)
+    w = W.small_random(9, shape, num_reqs=8, max_len=200, extra_slots=0)
+    w.num_slots = len(w.prestage_chunks) + 3                  # only three free slots
+    g, o = _pair(w)
+    sg, so = g.run_pass(validate=True), o.run_pass()
+    _compare_pass(g, o, sg, so)
+    assert sg.num_store == 3 and sg.dropped > 0
+
+
+# ---------------------------------------------------------------------------
+# kernels one by one, edge cases
+# ---------------------------------------------------------------------------
+
+def _hash_gpu(toks, tok_off, seed):
+    blk_off = oracle.block_offsets(tok_off)
+    d_t = torch.from_numpy(toks if toks.size else np.zeros(1, np.int32)).cuda()
+    d_o = torch.from_numpy(tok_off).cuda()
+    d_b = torch.from_numpy(blk_off).cuda()
+    out = torch.zeros(max(int(blk_off[-1]), 1), dtype=torch.int64, device="cuda")
+    kv.kv_hash_prefix(d_t, d_o, tok_off.size - 1, seed, d_b, out)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()[:int(blk_off[-1])].view(np.uint64)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 0xFFFFFFFFFFFFFFFF, 0x0123456789ABCDEF])
+def test_hash_ragged_lengths(seed):
+    rng = np.random.default_rng(seed & 0xFFFF)
+    lengths = list(range(0, 70)) + [255, 256, 257, 4095, 4096, 4097, 4112, 20000, 16 * 513]
+    toks = rng.integers(-2**31, 2**31, sum(lengths), dtype=np.int64).astype(np.int32)
+    tok_off = np.zeros(len(lengths) + 1, np.int64)
+    np.cumsum(lengths, out=tok_off[1:])
+    assert np.array_equal(_hash_gpu(toks, tok_off, seed), oracle.hash_prefix(toks, tok_off, seed))
+
+
+def test_hash_many_requests():
+    rng = np.random.default_rng(5)
+    lengths = rng.integers(0, 700, 3000)
+    toks = rng.integers(0, 32000, int(lengths.sum())).astype(np.int32)
+    tok_off = np.zeros(lengths.size + 1, np.int64)
+    np.cumsum(lengths, out=tok_off[1:])
+    assert np.array_equal(_hash_gpu(toks, tok_off, 3), oracle.hash_prefix(toks, tok_off, 3))
+
+
+def test_hash_empty_batch():
+    kv.kv_hash_prefix(torch.zeros(1, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.int64, device="cuda"),
+                      0, 0, torch.zeros(1, dtype=torch.int64, device="cuda"),
+                      torch.zeros(1, dtype=torch.int64, device="cuda"))
+    torch.cuda.synchronize()
+
+
+def _lookup_gpu(idx, bh, blk_off, bpc):
+    chunk_off = oracle.chunk_offsets(blk_off, bpc)
+    R = blk_off.size - 1
+    d_bh = torch.from_numpy(bh.view(np.int64) if bh.size else np.zeros(1, np.int64)).cuda()
+    cs = torch.full((max(int(chunk_off[-1]), 1),), -7, dtype=torch.int32, device="cuda")
+    hit = torch.full((max(R, 1),), -7, dtype=torch.int32, device="cuda")
+    kv.kv_lookup(idx, d_bh, torch.from_numpy(blk_off).cuda(), R, bpc, torch.from_numpy(chunk_off).cuda(), cs, hit)
+    torch.cuda.synchronize()
+    return cs.cpu().numpy()[:int(chunk_off[-1])], hit.cpu().numpy()[:R]
+
+
+def test_lookup_long_runs_cross_wave_width():
+    rng = np.random.default_rng(11)
+    base = rng.integers(0, 32000, 16 * 200).astype(np.int32)
+    reqs = [base, base[:16 * 64], base[:16 * 65], base[:16 * 63 + 5], base[:16 * 130], np.zeros(0, np.int32)]
+    tok_off = np.zeros(len(reqs) + 1, np.int64)
+    np.cumsum([r.size for r in reqs], out=tok_off[1:])
+    toks = np.concatenate(reqs)
+    bh = oracle.hash_prefix(toks, tok_off)
+    blk_off = oracle.block_offsets(tok_off)
+    keys = bh[blk_off[0]:blk_off[1]]
+    idx = kv.KvIndex(400)
+    ref = {}
+    for n_idx in [0, 63, 64, 65, 128, 129, 200]:
+        present = {int(k): i for i, k in enumerate(keys[:n_idx])}
+        present[int(keys[150])] = 150                       # present after a miss for some requests
+        add = {k: v for k, v in present.items() if k not in ref}
+        if add:
+            idx.insert(np.array(list(add.keys()), np.uint64), np.array(list(add.values()), np.int32))
+            ref.update(add)
+        cs, hit = _lookup_gpu(idx, bh, blk_off, 1)
+        ocs, ohit = oracle.lookup(ref, bh, blk_off, 1)
+        assert np.array_equal(cs, ocs) and np.array_equal(hit, ohit)
+    idx.destroy()
+
+
+def test_index_insert_erase_churn():
+    rng = np.random.default_rng(12)
+    toks = rng.integers(0, 32000, 16 * 3000).astype(np.int32)
+    tok_off = np.array([0, toks.size], np.int64)
+    bh = oracle.hash_prefix(toks, tok_off)
+    blk_off = oracle.block_offsets(tok_off)
+    keys = bh.copy()
+    idx = kv.KvIndex(300)
+    ref = {}
+    for it in range(60):
+        add = rng.choice(keys.size, 40, replace=False)
+        cand = {int(keys[i]): int(rng.integers(0, 1000)) for i in add}
+        room = 300 - len(ref)
+        items = [(k, v) for k, v in cand.items() if k in ref] + \
+                [(k, v) for k, v in cand.items() if k not in ref][:max(room, 0)]
+        if items:
+            idx.insert(np.array([k for k, _ in items], np.uint64), np.array([v for _, v in items], np.int32))
+            ref.update(items)
+        if ref:
+            live = list(ref.keys())
+            gone = [live[i] for i in rng.choice(len(live), min(len(live), 30), replace=False)]
+            idx.erase(np.array(gone, np.uint64))
+            for k in gone:
+                ref.pop(k)
+        assert idx.size() == len(ref)
+        cs, hit = _lookup_gpu(idx, bh, blk_off, 1)
+        ocs, ohit = oracle.lookup(ref, bh, blk_off, 1)
+        assert np.array_equal(cs, ocs) and np.array_equal(hit, ohit)
+    with pytest.raises(kv.KvError) as e:
+        fresh = [int(k) for k in keys if int(k) not in ref][:400]
+        idx.insert(np.array(fresh, np.uint64), np.zeros(len(fresh), np.int32))
+    assert e.value.status == kv.KV_ENOSPC
+    idx.destroy()
+
+
+def test_out_of_range_jobs_are_skipped_on_device():
+    shape = W.KVShape(2, 2, 64, 2, 16, 64)
+    w = W.small_random(21, shape, num_reqs=4, max_len=256)
+    g, o = _pair(w)
+    bt = w.block_tables.copy()
+    bt[0, 1] = -1
+    bt[0, 2] = w.num_blocks + 5
+    d_bt = torch.from_numpy(bt).cuda()
+    jobs = np.array([[-1, 0, 0, 0], [w.num_slots, 0, 0, 0], [0, -1, 0, 0], [0, w.num_reqs, 0, 0],
+                     [0, 0, -1, 0], [0, 0, bt.shape[1], 0], [1, 0, 0, 0]], np.int32)
+    d_jobs = torch.from_numpy(jobs).cuda()
+    kv.kv_retrieve_scatter(g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs, d_jobs, len(jobs))
+    oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs)
+    kv.kv_store_gather(g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs, d_jobs, len(jobs))
+    oracle.store_gather(o.layout, o.staging, o.layers, bt, jobs)
+    torch.cuda.synchronize()
+    assert np.array_equal(g.staging.cpu().numpy(), o.staging)
+    for l in range(2):
+        assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
+
+
+def test_zero_jobs_enqueue_nothing():
+    shape = W.KVShape(1, 2, 64, 2, 16, 64)
+    w = W.small_random(22, shape, num_reqs=2, max_len=128)
+    g, _ = _pair(w)
+    before = [t.clone() for t in g.layers]
+    kv.kv_retrieve_scatter(g.layout, g.staging, g.layers, g.bt, w.bt_stride, w.num_reqs, None, 0)
+    torch.cuda.synchronize()
+    assert all(torch.equal(a, b) for a, b in zip(before, g.layers))

@@ -24,7 +24,10 @@ Randomness:
 """
 from __future__ import annotations
 
+import ctypes
 import math
+import os
+import subprocess
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional, Sequence, Tuple
 
@@ -67,17 +70,82 @@ def _keys(tag: int, seed: int) -> Tuple[int, int]:
     return k1, k2
 
 
-def kv_words_np(tag: int, seed: int, start: int, count: int, finite: bool = True) -> np.ndarray:
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_FILL_SRC = os.path.join(_HERE, "kvfill.c")
+_FILL_LIB = os.path.join(_HERE, "libkvfill.so")
+_fill_lib = None
+
+
+def build_fill_lib() -> str:
+    """Compile the host form of the KV formula (always recompiles)."""
+    tmp = _FILL_LIB + ".tmp"
+    subprocess.check_call(["gcc", "-O3", "-std=c11", "-fPIC", "-shared", "-o", tmp, _FILL_SRC])
+    os.replace(tmp, _FILL_LIB)
+    return _FILL_LIB
+
+
+def _fill():
+    global _fill_lib
+    if _fill_lib is None:
+        if not os.path.exists(_FILL_LIB) or os.path.getmtime(_FILL_LIB) < os.path.getmtime(_FILL_SRC):
+            build_fill_lib()
+        lib = ctypes.CDLL(_FILL_LIB)
+        lib.kvfill_words.restype = None
+        lib.kvfill_words.argtypes = [ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64, ctypes.c_uint64,
+                                     ctypes.c_int, ctypes.c_void_p]
+        _fill_lib = lib
+    return _fill_lib
+
+
+def kv_words_np(tag: int, seed: int, start: int, count: int, finite: bool = True,
+                out: Optional[np.ndarray] = None) -> np.ndarray:
     """uint32 words [start, start+count) of buffer ``tag`` (host form)."""
     k1, k2 = _keys(tag, seed)
-    idx = np.arange(start, start + count, dtype=np.uint64)
-    lo = (idx & np.uint64(M32)).astype(np.uint32)
-    hi = (idx >> np.uint64(32)).astype(np.uint32)
-    chi = _fmix32_np((hi + np.uint32(k2)).astype(np.uint32))
-    v = _fmix32_np(_fmix32_np(lo ^ np.uint32(k1)) ^ chi)
-    if finite:
-        v &= np.uint32(FINITE_MASK)
-    return v
+    if out is None:
+        out = np.empty(count, np.uint32)
+    assert out.dtype == np.uint32 and out.flags.c_contiguous and out.size >= count
+    if count:
+        _fill().kvfill_words(k1, k2, start, count, 1 if finite else 0, out.ctypes.data)
+    return out
+
+
+def kv_words_np_reference(tag: int, seed: int, start: int, count: int, finite: bool = True) -> np.ndarray:
+    """The same words computed with numpy alone (slow; cross-checks the C form)."""
+    k1, k2 = _keys(tag, seed)
+    out = np.empty(count, np.uint32)
+    step = 1 << 16
+    tmp = np.empty(min(step, max(count, 1)), np.uint32)
+    pos = 0
+    while pos < count:
+        idx0 = start + pos
+        hi = idx0 >> 32
+        n = min(step, count - pos, (1 << 32) - (idx0 & M32))
+        chi = _fmix32_int((hi + k2) & M32)
+        v = out[pos:pos + n]
+        t = tmp[:n]
+        np.add(_RAMP[:n], np.uint32(idx0 & M32), out=v, casting="unsafe")
+        v ^= np.uint32(k1)
+        _fmix32_inplace(v, t)
+        v ^= np.uint32(chi)
+        _fmix32_inplace(v, t)
+        if finite:
+            v &= np.uint32(FINITE_MASK)
+        pos += n
+    return out
+
+
+_RAMP = np.arange(1 << 16, dtype=np.uint32)
+
+
+def _fmix32_inplace(x: np.ndarray, t: np.ndarray) -> None:
+    np.right_shift(x, 16, out=t)
+    x ^= t
+    x *= np.uint32(0x85EBCA6B)
+    np.right_shift(x, 13, out=t)
+    x ^= t
+    x *= np.uint32(0xC2B2AE35)
+    np.right_shift(x, 16, out=t)
+    x ^= t
 
 
 def kv_bytes_np(tag: int, seed: int, byte_start: int, nbytes: int, finite: bool = True) -> np.ndarray:
@@ -99,19 +167,22 @@ def _fmix32_t(x):
     return x ^ (x >> 16)
 
 
-def fill_kv_(buf, tag: int, seed: int, finite: bool = True, chunk_words: int = 1 << 25) -> None:
+def fill_kv_(buf, tag: int, seed: int, finite: bool = True, chunk_words: int = 1 << 25,
+             byte_start: int = 0) -> None:
     """Fill a torch uint8 tensor (any device, numel % 4 == 0) with the formula.
 
-    Words are numbered from the start of ``buf``; the result equals
-    ``kv_bytes_np(tag, seed, 0, buf.numel())`` byte for byte."""
+    ``buf`` receives bytes [byte_start, byte_start + numel) of buffer ``tag``:
+    the result equals ``kv_bytes_np(tag, seed, byte_start, buf.numel())``."""
     import torch
     assert buf.dtype == torch.uint8 and buf.numel() % 4 == 0 and buf.is_contiguous()
+    assert byte_start % 4 == 0
     words = buf.view(torch.int32)
     n = words.numel()
+    w0 = byte_start // 4
     k1, k2 = _keys(tag, seed)
     for s in range(0, n, chunk_words):
         e = min(n, s + chunk_words)
-        idx = torch.arange(s, e, device=buf.device, dtype=torch.int64)
+        idx = torch.arange(w0 + s, w0 + e, device=buf.device, dtype=torch.int64)
         lo = idx & M32
         hi = idx >> 32
         chi = _fmix32_t((hi + k2) & M32)
