@@ -84,6 +84,35 @@ def _cpu_baseline(shape_name: str):
                        f"{moved / 2**30:.1f} GiB moved in {dt:.2f} s, single-threaded C")}
 
 
+def _calibration_copy(torch, reps: int = 5) -> dict:
+    """A plain contiguous copy of known size, run by the library's own copy
+    kernel: one layer, block size == chunk size, block_first paged layout and
+    an identity block table make the retrieve scatter a 4 GiB memcpy (the
+    paged block [2][B][H][D] and the staged chunk [1][2][C][H][D] are the same
+    bytes).  Used to scale hardware byte counters.  Launches no other kernel."""
+    import numpy as np
+    import paper_2609_35065_amd as kv
+    n, seg = 4096, 256 * 8 * 128 * 2          # 4096 slots of 1 MiB; segment = one plane of a chunk
+    lo = kv.make_layout(1, 8, 128, 2, 256, 256, n, n, seg, 2 * seg)
+    stg = torch.empty(n * 2 * seg, dtype=torch.uint8, device="cuda")
+    pool = torch.empty(n * 2 * seg, dtype=torch.uint8, device="cuda")
+    bt = torch.from_numpy(np.arange(n, dtype=np.int32).reshape(n, 1)).cuda()
+    jobs = torch.from_numpy(np.stack([np.arange(n), np.arange(n), np.zeros(n), np.zeros(n)], 1)
+                            .astype(np.int32)).cuda()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    kv.kv_retrieve_scatter(lo, stg, [pool], bt, 1, n, jobs, n)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        kv.kv_retrieve_scatter(lo, stg, [pool], bt, 1, n, jobs, n)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    return {"calibration": "contiguous copy by kv_copy_retrieve", "bytes_read_per_dispatch": n * 2 * seg,
+            "bytes_written_per_dispatch": n * 2 * seg, "dispatches": reps + 1, "ms": round(ms, 4),
+            "GB/s_rw": round(2 * n * 2 * seg / (ms * 1e-3) / 1e9, 1)}
+
+
 def _device_copy_gbs(torch, nbytes: int = 4 << 30, reps: int = 5) -> float:
     """Plain device-to-device copy rate (read + write bytes / time): practical-peak context."""
     a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -111,7 +140,10 @@ def main() -> int:
     ap.add_argument("--workload", default="l32-64x4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
-                    help="only run a plain 4 GiB device copy 5 times (counter calibration) and exit")
+                    help="only run a plain 4 GiB contiguous copy (counter calibration) and exit")
+    ap.add_argument("--no-fill", action="store_true",
+                    help="leave KV buffers uninitialised (hardware-counter runs: no generator kernels run; the "
+                         "copies move the same bytes) and skip the device-copy and CPU-baseline extras")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -130,15 +162,15 @@ def main() -> int:
         return 2
     torch.cuda.set_device(0)
     if args.calib_copy:
-        gbs = _device_copy_gbs(torch)
-        print(json.dumps({"calibration": "device copy", "bytes_per_dispatch": 4 << 30, "gbs_rw": round(gbs, 1)}))
+        print(json.dumps(_calibration_copy(torch)))
         return 0
 
     w = W.make(args.workload)
     print(f"[bench] workload {w.name}: {w.num_reqs} requests, pool {w.pool_bytes() / 2**30:.1f} GiB, "
           f"staging {w.staged_bytes() / 2**30:.1f} GiB", file=sys.stderr, flush=True)
     path = StagingPath(w)
-    path.fill(STG_TAG, POOL_TAG, w.seed)
+    if not args.no_fill:
+        path.fill(STG_TAG, POOL_TAG, w.seed)
     path.prestage()
     for _ in range(args.warmup):
         path.run_pass(evict_stored=True)
@@ -209,8 +241,9 @@ def main() -> int:
     del path
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    line["device_copy_GB/s"] = round(_device_copy_gbs(torch), 1)
-    if not args.no_cpu_baseline:
+    if not args.no_fill:
+        line["device_copy_GB/s"] = round(_device_copy_gbs(torch), 1)
+    if not args.no_cpu_baseline and not args.no_fill:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = _cpu_baseline("l80" if w.shape.num_layers == 80 else "l32")
     print(json.dumps(line), flush=True)

@@ -87,12 +87,12 @@ class StagingPath:
             self.tok_off = torch.from_numpy(w.tok_off).to(d)
             self.blk_off = torch.from_numpy(blk_off).to(d)
             self.chunk_off = torch.from_numpy(chunk_off).to(d)
-            self.block_hash = torch.zeros(max(nblk, 1), dtype=torch.int64, device=d)
-            self.chunk_slot = torch.zeros(max(nch, 1), dtype=torch.int32, device=d)
-            self.hit = torch.zeros(max(R, 1), dtype=torch.int32, device=d)
+            self.block_hash = torch.empty(max(nblk, 1), dtype=torch.int64, device=d)
+            self.chunk_slot = torch.empty(max(nch, 1), dtype=torch.int32, device=d)
+            self.hit = torch.empty(max(R, 1), dtype=torch.int32, device=d)
             self.bt = torch.from_numpy(np.ascontiguousarray(w.block_tables)).to(d)
-            self.d_retr = torch.zeros((max(nch, 1), 4), dtype=torch.int32, device=d)
-            self.d_store = torch.zeros((max(nch, 1), 4), dtype=torch.int32, device=d)
+            self.d_retr = torch.empty((max(nch, 1), 4), dtype=torch.int32, device=d)
+            self.d_store = torch.empty((max(nch, 1), 4), dtype=torch.int32, device=d)
         # pinned host mirrors for the one D2H and one H2D copy of a pass
         self.h_block_hash = torch.zeros(max(nblk, 1), dtype=torch.int64, pin_memory=True)
         self.h_chunk_slot = torch.zeros(max(nch, 1), dtype=torch.int32, pin_memory=True)
@@ -141,7 +141,7 @@ class StagingPath:
                 dt = torch.from_numpy(toks if toks.size else np.zeros(1, np.int32)).to(self.dev)
                 doff = torch.from_numpy(off).to(self.dev)
                 dboff = torch.from_numpy(boff).to(self.dev)
-                dh = torch.zeros(max(int(boff[-1]), 1), dtype=torch.int64, device=self.dev)
+                dh = torch.empty(max(int(boff[-1]), 1), dtype=torch.int64, device=self.dev)
                 kv_hash_prefix(dt, doff, off.size - 1, self.hash_seed, dboff, dh, self.stream)
                 h = dh.cpu().numpy().view(np.uint64)
             keys = np.array([h[boff[p] + (j + 1) * self.bpc - 1] for p, j in w.prestage_chunks], np.uint64)
