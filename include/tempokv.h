@@ -204,6 +204,13 @@ int kv_store_gather(const kv_layout *layout, void *d_staging, const void *const 
                     const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
                     const kv_job *d_jobs, int32_t num_jobs, void *stream);
 
+/* Reorder a job list in host memory so that jobs naming the same staging
+ * slot are adjacent (stable: by slot, then original order).  The copies'
+ * results do not depend on job order (destinations are disjoint within a
+ * call); the retrieve kernel reads a staged chunk once per unit when the
+ * jobs sharing it run back to back.  Errors: KV_EINVAL. */
+int kv_group_jobs_by_slot(kv_job *h_jobs, int32_t num_jobs);
+
 /* Host check of a job batch against copies of its tables: KV_ERANGE if any
  * slot, request, chunk or (valid-job) block id is out of range or any
  * reserved field is non-zero, KV_EDUP if two jobs write the same destination

@@ -26,7 +26,7 @@ HASH_BLOCK_TOKENS = 16
 # every symbol include/tempokv.h declares
 EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
            "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
-           "kv_store_gather", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
+           "kv_store_gather", "kv_group_jobs_by_slot", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
            "kv_host_device_pointer", "kv_version"]
 
 
@@ -72,6 +72,7 @@ def lib() -> ct.CDLL:
                           ct.POINTER(_i32), ct.POINTER(_i32)],
         "kv_retrieve_scatter": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
         "kv_store_gather": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
+        "kv_group_jobs_by_slot": [_vp, _i32],
         "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
         "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
         "kv_strerror": [ct.c_int],
@@ -289,6 +290,13 @@ def kv_store_gather(layout: KvLayout, d_staging, layers: Sequence, d_block_table
                                  _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
                                  _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
                                  _stream(stream)), "kv_store_gather")
+
+
+def kv_group_jobs_by_slot(jobs: np.ndarray) -> np.ndarray:
+    """Returns the jobs ([n,4] int32) stably ordered by slot (a copy)."""
+    jb = np.ascontiguousarray(jobs, np.int32).reshape(-1, 4).copy()
+    _check(lib().kv_group_jobs_by_slot(jb.ctypes.data if jb.size else None, jb.shape[0]), "kv_group_jobs_by_slot")
+    return jb
 
 
 def kv_validate_jobs(layout: KvLayout, block_tables: np.ndarray, jobs: np.ndarray, is_store: bool) -> int:

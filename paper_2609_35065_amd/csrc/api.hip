@@ -4,6 +4,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
 #include <unordered_set>
 #include <vector>
 
@@ -154,6 +155,12 @@ int kv_build_jobs(const int32_t *h_hit_chunks, const int32_t *h_chunk_slot, cons
     *num_store = ns;
     *dropped = nd;
     return nd > 0 ? KV_ENOSPC : KV_OK;
+}
+
+int kv_group_jobs_by_slot(kv_job *h_jobs, int32_t num_jobs) {
+    if (num_jobs < 0 || (num_jobs > 0 && !h_jobs)) return KV_EINVAL;
+    std::stable_sort(h_jobs, h_jobs + num_jobs, [](const kv_job &a, const kv_job &b) { return a.slot < b.slot; });
+    return KV_OK;
 }
 
 int kv_validate_jobs(const kv_layout *layout, const int32_t *h_block_tables, int32_t bt_stride, int32_t num_reqs,

@@ -12,11 +12,11 @@
 // The unit's staged bytes are read front to back in stages of 8 vectors per
 // lane and the stages are software-pipelined: the loads of stage s+1 are in
 // flight while stage s is stored.  Block ids come through the scalar cache.
-// Units are ordered (layer, plane)-major and job-minor, so the jobs that
-// share a staged chunk (requests reusing one prefix) read the same 512 KiB
-// in a short window served by L2 / the Infinity Cache: measured HBM reads
-// equal the unique staged bytes, not the per-job payload.  Loads are cached;
-// paged writes are non-temporal.
+// Units are ordered (layer, plane)-major and job-minor, and each of the 8
+// XCDs walks one contiguous range of that order, so the jobs that share a
+// staged chunk (requests reusing one prefix; adjacent once the job list is
+// grouped by slot) read the same 512 KiB back to back through one XCD's L2.
+// Loads are cached; paged writes are non-temporal.
 //
 // Store (paged -> staging), fast path: 1024-lane workgroups, each copying a
 // group of segments with 16 vectors per lane in flight (256 KiB per
@@ -59,6 +59,10 @@ __device__ __forceinline__ bool blk_ok(const CopyParams &p, int32_t blk) {
     return blk >= 0 && blk < p.num_blocks;
 }
 
+// Accelerator complex dies on MI355X; consecutive workgroups of a launch are
+// dispatched to them round-robin.  Only performance depends on this value.
+constexpr int kXcds = 8;
+
 // --------------------------------------------------------------------------
 // Retrieve fast path: R rows of 4 KiB per segment (segment = R * 4 KiB).
 // --------------------------------------------------------------------------
@@ -69,8 +73,14 @@ __global__ __launch_bounds__(256) void retrieve_unit_kernel(CopyParams p) {
     constexpr int V = R * SB;                // vectors per lane per stage
     const int tid = threadIdx.x;
     const int64_t units = (int64_t)p.num_jobs * p.L * 2;
+    const int64_t per_xcd = (units + kXcds - 1) / kXcds;
     const int32_t nstage = (p.nseg + SB - 1) / SB;
-    for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
+    // XCD-aware order: workgroup b runs on XCD b mod 8, so XCD x walks the
+    // contiguous range [x*per_xcd, (x+1)*per_xcd) of the unit order; the
+    // grid (and its stride) is a multiple of kXcds.
+    for (int64_t w = blockIdx.x; w < per_xcd * kXcds; w += gridDim.x) {
+        const int64_t u = (w % kXcds) * per_xcd + w / kXcds;
+        if (u >= units) continue;
         const int64_t q = u % p.num_jobs;
         const int64_t t = u / p.num_jobs;
         const int32_t kv = (int32_t)(t & 1);
@@ -208,7 +218,9 @@ unsigned grid_of(int64_t items) { return (unsigned)(items < kMaxGrid ? items : k
 
 template <int R>
 void launch_retrieve_unit(const CopyParams &p, hipStream_t s) {
-    hipLaunchKernelGGL(retrieve_unit_kernel<R>, dim3(grid_of((int64_t)p.num_jobs * p.L * 2)), dim3(256), 0, s, p);
+    const int64_t units = (int64_t)p.num_jobs * p.L * 2;
+    const int64_t grid = (units + kXcds - 1) / kXcds * kXcds;   // kMaxGrid is a multiple of kXcds too
+    hipLaunchKernelGGL(retrieve_unit_kernel<R>, dim3(grid_of(grid)), dim3(256), 0, s, p);
 }
 
 template <int T, int R>

@@ -19,8 +19,8 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, kv_build_jobs, kv_commit_should_stage, kv_hash_prefix,
-               kv_host_device_pointer, kv_lookup, kv_retrieve_scatter, kv_store_gather, make_layout)
+from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, kv_build_jobs, kv_commit_should_stage, kv_group_jobs_by_slot,
+               kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_scatter, kv_store_gather, make_layout)
 
 
 @dataclass
@@ -196,7 +196,8 @@ class StagingPath:
         nr, ns = len(retr), len(store)
         with torch.cuda.stream(self.stream):
             if nr:
-                self.h_retr.numpy()[:nr] = retr
+                # jobs sharing a staged chunk run back to back (results do not depend on order)
+                self.h_retr.numpy()[:nr] = kv_group_jobs_by_slot(retr)
                 self.d_retr[:nr].copy_(self.h_retr[:nr], non_blocking=True)
             if ns:
                 self.h_store.numpy()[:ns] = store

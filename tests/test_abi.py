@@ -164,3 +164,14 @@ def test_hash_and_lookup_argument_checks():
     assert L.kv_index_destroy(None) == kv.KV_EINVAL
     assert L.kv_index_insert(None, None, None, 0, None) == kv.KV_EINVAL
     assert L.kv_host_device_pointer(None, ct.byref(ct.c_void_p())) == kv.KV_EINVAL
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_group_jobs_by_slot_is_a_stable_sort(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(0, 300))
+    jobs = np.stack([rng.integers(0, 20, n), np.arange(n), rng.integers(0, 4, n), np.zeros(n, np.int64)], 1).astype(np.int32)
+    got = kv.kv_group_jobs_by_slot(jobs)
+    want = jobs[np.argsort(jobs[:, 0], kind="stable")]
+    assert np.array_equal(got, want)
+    assert kv.lib().kv_group_jobs_by_slot(None, -1) == kv.KV_EINVAL
