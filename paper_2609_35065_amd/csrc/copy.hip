@@ -21,8 +21,9 @@
 // Store (paged -> staging), fast path: 1024-lane workgroups, each copying a
 // group of segments with 16 vectors per lane in flight (256 KiB per
 // workgroup for 32 KiB segments), all loads before all stores; job-major
-// order so consecutive workgroups fill one staging slot front to back.  Both
-// loads and stores are non-temporal: each byte is touched once.
+// order, each XCD taking one contiguous range of it, so a die fills whole
+// staging slots front to back.  Both loads and stores are non-temporal: each
+// byte is touched once.
 //
 // On MI355X these shapes were chosen by measurement: at 256 lanes a plain
 // contiguous copy tops out near 5.2 TB/s (read + write), at 1024 lanes near
@@ -131,7 +132,12 @@ __global__ __launch_bounds__(T) void store_group_kernel(CopyParams p) {
     const int tid = threadIdx.x;
     const int32_t gpu = (p.nseg + SPW - 1) / SPW;
     const int64_t total = (int64_t)p.num_jobs * p.L * 2 * gpu;
-    for (int64_t g = blockIdx.x; g < total; g += gridDim.x) {
+    const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+    // XCD x copies the contiguous range [x*per_xcd, (x+1)*per_xcd) of the
+    // job-major group order: whole staging slots per die.
+    for (int64_t w = blockIdx.x; w < per_xcd * kXcds; w += gridDim.x) {
+        const int64_t g = (w % kXcds) * per_xcd + w / kXcds;
+        if (g >= total) continue;
         const int32_t ig = (int32_t)(g % gpu);
         int64_t t = g / gpu;
         const int32_t kv = (int32_t)(t & 1);
@@ -226,7 +232,8 @@ void launch_retrieve_unit(const CopyParams &p, hipStream_t s) {
 template <int T, int R>
 void launch_store_group(const CopyParams &p, hipStream_t s) {
     const int64_t gpu = (p.nseg + 16 / R - 1) / (16 / R);
-    hipLaunchKernelGGL((store_group_kernel<T, R>), dim3(grid_of((int64_t)p.num_jobs * p.L * 2 * gpu)), dim3(T), 0,
+    const int64_t total = (int64_t)p.num_jobs * p.L * 2 * gpu;
+    hipLaunchKernelGGL((store_group_kernel<T, R>), dim3(grid_of((total + kXcds - 1) / kXcds * kXcds)), dim3(T), 0,
                        s, p);
 }
 

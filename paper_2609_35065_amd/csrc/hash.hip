@@ -2,9 +2,10 @@
 //
 // Hash.  h_{-1} = seed, h_b = M(h_{b-1} ^ d_b ^ G), d_b = sum_j M(word(j, tok))
 // over the 16 tokens of block b, M = SplitMix64's finalizer.  The digests are
-// independent and computed one block per lane; the chain is sequential and
-// runs on one lane per request, fed from LDS.  One 256-lane workgroup per
-// request walks its blocks in tiles of 256.
+// independent and computed one block per lane; the chain is sequential, so
+// its latency sets the rate: it runs on the scalar ALU of one wave per
+// request (a step is ~20 scalar instructions: two xor-shift-multiply rounds
+// on 32-bit halves), while the workgroup's other waves digest the next tile.
 //
 // Lookup.  One wave per request probes up to 64 chunk keys at once in the
 // device open-addressing table and turns the 64 hit flags into the length of
@@ -16,6 +17,7 @@ namespace tkv {
 namespace {
 
 constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+constexpr int kWave = 64;
 constexpr int kHashThreads = 256;
 
 __device__ __forceinline__ uint64_t mix64(uint64_t z) {
@@ -24,38 +26,119 @@ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
     return z ^ (z >> 31);
 }
 
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int lane) {
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, lane);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Lane K of `old` takes the wave-uniform value `val` (v_writelane_b32 with
+// an inline-constant lane number); the other lanes keep theirs.
+template <int K>
+__device__ __forceinline__ uint32_t writelane(uint32_t old, uint32_t val) {
+    asm("v_writelane_b32 %0, %1, %2" : "+v"(old) : "s"(val), "n"(K));
+    return old;
+}
+
+// Steps K..K+7 of the chain over a full group of 64 blocks, unrolled so that
+// every lane number is an immediate.  The eight digests are read into scalar
+// registers before the eight dependent steps, keeping v_readlane latency off
+// the chain.
+template <int K>
+struct ChainGroup {
+    static __device__ __forceinline__ void run(uint64_t &h, uint64_t d, uint32_t &lo, uint32_t &hi) {
+        uint64_t dk[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dk[j] = readlane64(d, K + j);
+        __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the steps
+        uint64_t hk[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            h = mix64(h ^ dk[j]);
+            hk[j] = h;
+        }
+        Park<K, 0>::run(hk, lo, hi);
+        ChainGroup<K + 8>::run(h, d, lo, hi);
+    }
+    template <int B, int J>
+    struct Park {
+        static __device__ __forceinline__ void run(const uint64_t *hk, uint32_t &lo, uint32_t &hi) {
+            lo = writelane<B + J>(lo, (uint32_t)hk[J]);
+            hi = writelane<B + J>(hi, (uint32_t)(hk[J] >> 32));
+            Park<B, J + 1>::run(hk, lo, hi);
+        }
+    };
+    template <int B>
+    struct Park<B, 8> {
+        static __device__ __forceinline__ void run(const uint64_t *, uint32_t &, uint32_t &) {}
+    };
+};
+template <>
+struct ChainGroup<64> {
+    static __device__ __forceinline__ void run(uint64_t &, uint64_t, uint32_t &, uint32_t &) {}
+};
+
+__device__ __forceinline__ uint64_t block_digest(const int32_t *tp) {
+    uint64_t d = 0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) d += mix64((uint64_t)(uint32_t)tp[j] + ((uint64_t)(j + 1) << 32));
+    return d ^ kGamma;   // the chain's constant, folded in here, off the chain
+}
+
+// One 256-lane workgroup per request, blocks in tiles of 256.  The digests
+// of a tile are independent: all four waves compute the first tile into LDS;
+// afterwards wave 0 runs the chain over tile t while waves 1-3 digest tile
+// t+1 into the other LDS buffer.  The chain runs with wave-uniform values, so
+// it executes on the scalar ALU: for each group of 64 blocks, lane k holds
+// digest k, v_readlane moves it to scalar registers, and v_writelane parks
+// h_k in lane k, which then stores the group's 64 hashes in one write.
 __global__ __launch_bounds__(kHashThreads) void hash_kernel(const int32_t *__restrict__ tokens,
-                                                          const int64_t *__restrict__ tok_off,
-                                                          uint64_t seed, const int64_t *__restrict__ blk_off,
-                                                          uint64_t *__restrict__ out) {
-    __shared__ uint64_t dig[kHashThreads];
+                                                           const int64_t *__restrict__ tok_off, uint64_t seed,
+                                                           const int64_t *__restrict__ blk_off,
+                                                           uint64_t *__restrict__ out) {
+    __shared__ uint64_t dig[2][kHashThreads];
     const int r = blockIdx.x;
     const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // wave-uniform by construction
+    const int lane = tid % kWave;
     const int64_t t0 = tok_off[r];
     const int64_t n = tok_off[r + 1] - t0;
     int64_t nb = n > 0 ? n / 16 : 0;
     const int64_t o0 = blk_off[r];
     const int64_t span = blk_off[r + 1] - o0;
     if (span < nb) nb = span > 0 ? span : 0;
+    const int64_t ntiles = (nb + kHashThreads - 1) / kHashThreads;
+    const int32_t *tk = tokens + t0;
 
-    uint64_t h = seed;
-    for (int64_t tile = 0; tile < nb; tile += kHashThreads) {
-        const int64_t b = tile + tid;
-        if (b < nb) {
-            const int32_t *tp = tokens + t0 + b * 16;
-            uint64_t d = 0;
-#pragma unroll
-            for (int j = 0; j < 16; ++j)
-                d += mix64((uint64_t)(uint32_t)tp[j] + ((uint64_t)(j + 1) << 32));
-            dig[tid] = d;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            const int64_t cnt = nb - tile < kHashThreads ? nb - tile : kHashThreads;
-            for (int64_t k = 0; k < cnt; ++k) {
-                h = mix64(h ^ dig[k] ^ kGamma);
-                out[o0 + tile + k] = h;
+    if (tid < nb) dig[0][tid] = block_digest(tk + (int64_t)tid * 16);
+    __syncthreads();
+    uint64_t h = seed;   // live in wave 0 only
+    for (int64_t t = 0; t < ntiles; ++t) {
+        const int64_t tb = t * kHashThreads;
+        if (wave == 0) {
+            const uint64_t *dt = dig[t & 1];
+            const int64_t left = nb - tb < kHashThreads ? nb - tb : kHashThreads;
+            for (int64_t g = 0; g < left; g += kWave) {
+                const uint64_t d = dt[g + lane];
+                uint32_t mine_lo = 0, mine_hi = 0;
+                if (left - g >= kWave) {
+                    ChainGroup<0>::run(h, d, mine_lo, mine_hi);
+                } else {                               // ragged last group
+                    const int cnt = (int)(left - g);
+                    uint64_t mine = 0;
+                    for (int k = 0; k < cnt; ++k) {
+                        h = mix64(h ^ readlane64(d, k));
+                        if (lane == k) mine = h;
+                    }
+                    mine_lo = (uint32_t)mine;
+                    mine_hi = (uint32_t)(mine >> 32);
+                }
+                if (g + lane < left) out[o0 + tb + g + lane] = ((uint64_t)mine_hi << 32) | mine_lo;
             }
+        } else if (t + 1 < ntiles) {
+            const int64_t nt = tb + kHashThreads;
+            for (int i = tid - kWave; i < kHashThreads; i += kHashThreads - kWave)
+                if (nt + i < nb) dig[(t + 1) & 1][i] = block_digest(tk + (nt + i) * 16);
         }
         __syncthreads();
     }
@@ -114,8 +197,8 @@ hipError_t launch_hash(const int32_t *tokens, const int64_t *tok_off, int32_t nu
                        const int64_t *blk_off, uint64_t *out, hipStream_t stream) {
     if (num_reqs <= 0) return hipSuccess;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(hash_kernel, dim3(num_reqs), dim3(kHashThreads), 0, stream, tokens, tok_off, seed,
-                       blk_off, out);
+    hipLaunchKernelGGL(hash_kernel, dim3(num_reqs), dim3(kHashThreads), 0, stream, tokens, tok_off, seed, blk_off,
+                       out);
     return hipGetLastError();
 }
 
