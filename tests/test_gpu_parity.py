@@ -301,3 +301,17 @@ def test_zero_jobs_enqueue_nothing():
     kv.kv_retrieve_scatter(g.layout, g.staging, g.layers, g.bt, w.bt_stride, w.num_reqs, None, 0)
     torch.cuda.synchronize()
     assert all(torch.equal(a, b) for a, b in zip(before, g.layers))
+
+
+@pytest.mark.parametrize("layout", ["kv_first", "block_first"])
+def test_host_staging_zero_copy(layout):
+    # Staging buffer in mapped pinned host memory, read and written by the
+    # kernels over the host link; every byte compared.
+    shape = W.KVShape(2, 8, 128, 2, 16, 64)
+    w = W.small_random(31, shape, num_reqs=6, max_len=400, paged_layout=layout)
+    w.staging_in_host = True
+    g, o = _pair(w)
+    assert g.staging is None and g.staging_host is not None
+    for p in range(2):
+        sg, so = g.run_pass(validate=True), o.run_pass()
+        _compare_pass(g, o, sg, so)
