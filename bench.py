@@ -135,6 +135,69 @@ def _calibration_copy(torch, reps: int = 5) -> dict:
             "GB/s_rw": round(2 * n * 2 * seg / (ms * 1e-3) / 1e9, 1)}
 
 
+def _controller_bench() -> dict:
+    """The claim/commitment controller simulation: the six policy
+    configurations of the paper's policy comparison on a request stream shaped
+    like its workload (three prefix ratios), plus the library's simulator
+    timed against the oracle's on one long shared-prefix stream."""
+    import numpy as np
+    import paper_2609_35065_amd as kv
+    import workloads as W
+    from oracle import controller as ct
+    GiB = float(1 << 30)
+    base = dict(budget=50 * GiB, capacity=100 * GiB, stage_rate=11 * GiB, static_rate=11 * GiB, gpu_rate=25 * GiB,
+                prefill_s=1e-4, decode_s=0.03, tick=0.05, max_active=4)
+    configs = [("Demand", kv.KV_POLICY_DEMAND, 0), ("Immediate", kv.KV_POLICY_IMMEDIATE, 0),
+               ("Queue-1", kv.KV_POLICY_QUEUE_K, 1), ("Queue-4", kv.KV_POLICY_QUEUE_K, 4),
+               ("TempoKV-Static", kv.KV_POLICY_TEMPO_STATIC, 0), ("TempoKV", kv.KV_POLICY_TEMPO, 0)]
+
+    def kcfg(policy, k, **over):
+        d = dict(base, **over)
+        return kv.KvSimConfig(d["budget"], d["capacity"], d["stage_rate"], d["static_rate"], d["gpu_rate"],
+                              d["prefill_s"], d["decode_s"], d["tick"], d["max_active"], policy, k, 0)
+
+    out = {"policies": {}, "capacity_sweep": {}}
+    for ratio in (0.5, 0.75, 1.0):
+        sc = W.policy_scenario(ratio)
+        rows = {}
+        for name, pol, k in configs:
+            res, ft, dn, _ = kv.kv_sim_run(kcfg(pol, k), sc.obj_bytes, sc.arrival, sc.manifests, sc.uncached,
+                                           sc.out_tokens)
+            ttft = np.array(ft) - np.array(sc.arrival)
+            tput = sum(sc.out_tokens) / (max(dn) - min(sc.arrival))
+            rows[name] = {"C_GiBs_per_req": round(res.cost_gib_s_per_request, 3),
+                          "p95_ttft_s": round(float(np.percentile(ttft, 95)), 3),
+                          "out_tok_per_s": round(tput, 2), "blocked": res.blocked, "ordinary": res.ordinary}
+        imm, tk = rows["Immediate"]["C_GiBs_per_req"], rows["TempoKV"]["C_GiBs_per_req"]
+        rows["TempoKV_C_reduction_vs_Immediate"] = round(1 - tk / imm, 3) if imm else None
+        out["policies"][f"ratio_{int(ratio * 100)}"] = rows
+    sc = W.policy_scenario(1.0)
+    for cap in (100, 50, 25):
+        rows = {}
+        for name, pol, k in configs:
+            res, ft, dn, _ = kv.kv_sim_run(kcfg(pol, k, capacity=cap * GiB, budget=cap / 2 * GiB), sc.obj_bytes,
+                                           sc.arrival, sc.manifests, sc.uncached, sc.out_tokens)
+            ttft = np.array(ft) - np.array(sc.arrival)
+            rows[name] = {"C_GiBs_per_req": round(res.cost_gib_s_per_request, 3),
+                          "p95_ttft_s": round(float(np.percentile(ttft, 95)), 3), "blocked": res.blocked}
+        out["capacity_sweep"][f"fast_tier_{cap}GiB"] = rows
+    # simulator speed: library vs oracle on the same long stream, same results
+    sc = W.shared_prefix_scenario(400)
+    c = ct.SimConfig(policy=ct.TEMPO, queue_k=4, **base)
+    t0 = time.perf_counter()
+    ref = ct.simulate(c, sc.obj_bytes, sc.arrival, sc.manifests, sc.uncached, sc.out_tokens)
+    t_py = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    res, ft, dn, _ = kv.kv_sim_run(kcfg(kv.KV_POLICY_TEMPO, 4), sc.obj_bytes, sc.arrival, sc.manifests, sc.uncached,
+                                   sc.out_tokens)
+    t_cc = time.perf_counter() - t0
+    assert res.area_byte_s == ref["area"], "simulator and oracle disagree"
+    out["simulator_speed"] = {"scenario": sc.name, "events": res.events, "library_s": round(t_cc, 4),
+                              "oracle_s": round(t_py, 3), "library_events_per_s": round(res.events / t_cc),
+                              "speedup": round(t_py / t_cc, 1)}
+    return out
+
+
 def _device_copy_gbs(torch, nbytes: int = 4 << 30, reps: int = 5) -> float:
     """Plain device-to-device copy rate (read + write bytes / time): practical-peak context."""
     a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -161,6 +224,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="l32-64x4096")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--controller", action="store_true",
+                    help="run the claim/commitment controller simulation (host only) and exit")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only run a plain 4 GiB contiguous copy (counter calibration) and exit")
     ap.add_argument("--no-fill", action="store_true",
@@ -173,6 +238,10 @@ def main() -> int:
         print("bench.py measures one GPU only: the staging path shards by request with no exchange between "
               "GPUs, so multi-GPU runs are not part of this benchmark (use --gpus 1).", file=sys.stderr)
         return 2
+
+    if args.controller:
+        print(json.dumps({"controller": _controller_bench()}))
+        return 0
 
     import numpy as np
     import torch

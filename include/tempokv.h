@@ -243,6 +243,68 @@ int kv_commit_should_stage(double ttu_s, double ttr_s, uint64_t free_protected_b
                            uint64_t budget_bytes, int retrieval_requested);
 
 /* ----------------------------------------------------------------------- */
+/* Claim controller and staging simulator (host)                            */
+/* ----------------------------------------------------------------------- */
+
+/* Commitment policies (Section 5, "Policies"): when a PLANNED claim becomes
+ * eligible for a commitment attempt.  Retrieval requested by the runtime makes
+ * any claim eligible. */
+typedef enum kv_policy {
+    KV_POLICY_DEMAND = 0,        /* only when retrieval is requested */
+    KV_POLICY_IMMEDIATE = 1,     /* as soon as the claim is reported */
+    KV_POLICY_QUEUE_K = 2,       /* when the request is among the first K waiting */
+    KV_POLICY_TEMPO_STATIC = 3,  /* TTU <= TTR, TTR = non-resident bytes / static rate, in isolation */
+    KV_POLICY_TEMPO = 4          /* TTU <= TTR, TTR from a projection of the staging queue */
+} kv_policy;
+
+/* Simulation of the controller (Section 3) with a runtime and staging-device
+ * model.  Fast tier of capacity_bytes with a protected budget; one FIFO
+ * staging server at stage_rate bytes/s; FCFS runtime with max_active slots;
+ * retrieval at gpu_rate bytes/s, then prefill_s per uncached token and
+ * decode_s per output token; control points after every event and every
+ * tick_s seconds.  Byte counts must be integers below 2^53. */
+typedef struct kv_sim_config {
+    double budget_bytes, capacity_bytes, stage_rate, static_rate, gpu_rate, prefill_s, decode_s, tick_s;
+    int32_t max_active, policy, queue_k, reserved;   /* reserved must be 0 */
+} kv_sim_config;
+
+typedef struct kv_sim_result {
+    double area_byte_s;            /* integral of reserved protected bytes P(t) over time */
+    double cost_gib_s_per_request; /* C = area / 2^30 / N (Section 5, "Metrics") */
+    double end_s;                  /* time the last request ended */
+    double p_max_bytes;            /* largest P(t) */
+    int32_t committed;             /* claims committed */
+    int32_t blocked;               /* requests whose claim was blocked by capacity at least once */
+    int32_t ordinary;              /* requests that took the ordinary (demand) path */
+    int32_t reserved;
+    int64_t events;                /* events processed */
+} kv_sim_result;
+
+typedef enum kv_sim_trace_kind {
+    KV_TR_ARRIVE = 0, KV_TR_ADMIT, KV_TR_COMMIT, KV_TR_ORDINARY, KV_TR_READY, KV_TR_STAGEREADY,
+    KV_TR_TRANSFER, KV_TR_FETCH, KV_TR_RELEASE, KV_TR_DONE, KV_TR_EVICT
+} kv_sim_trace_kind;
+
+typedef struct kv_sim_event {
+    double t;
+    int32_t kind;   /* kv_sim_trace_kind */
+    int32_t id;     /* request id, or object id for READY / EVICT */
+} kv_sim_event;
+
+/* Run one simulation.  Objects 0..num_objects-1 have h_obj_bytes[o] bytes;
+ * request i arrives at h_arrival[i] (non-decreasing not required), needs the
+ * objects h_manifest_objs[h_manifest_off[i] .. h_manifest_off[i+1]) in that
+ * order, and has h_uncached[i] uncached and h_out_tokens[i] output tokens.
+ * Outputs: first-token and end times per request, the result summary, and
+ * (optional, h_trace may be NULL) the event trace, truncated to trace_cap
+ * entries with *trace_len the full length.  Errors: KV_EINVAL. */
+int kv_sim_run(const kv_sim_config *cfg, const double *h_obj_bytes, int32_t num_objects,
+               const double *h_arrival, const int64_t *h_manifest_off, const int32_t *h_manifest_objs,
+               const int32_t *h_uncached, const int32_t *h_out_tokens, int32_t num_requests,
+               double *h_first_token, double *h_done, kv_sim_result *result, kv_sim_event *h_trace,
+               int64_t trace_cap, int64_t *trace_len);
+
+/* ----------------------------------------------------------------------- */
 /* Misc                                                                     */
 /* ----------------------------------------------------------------------- */
 

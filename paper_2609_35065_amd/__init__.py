@@ -20,6 +20,9 @@ LIB_PATH = os.path.join(_HERE, "libtempokv.so")
 
 KV_OK, KV_EINVAL, KV_EALIGN, KV_ERANGE, KV_ENOSPC, KV_EHIP, KV_EDUP = 0, -1, -2, -3, -4, -5, -6
 KV_DEFER, KV_COMMIT, KV_BLOCKED, KV_ORDINARY = 0, 1, 2, 3
+KV_POLICY_DEMAND, KV_POLICY_IMMEDIATE, KV_POLICY_QUEUE_K, KV_POLICY_TEMPO_STATIC, KV_POLICY_TEMPO = range(5)
+SIM_TRACE_KINDS = ["arrive", "admit", "commit", "ordinary", "ready", "stageready", "transfer", "fetch", "release",
+                   "done", "evict"]
 KV_MAX_LAYERS = 128
 HASH_BLOCK_TOKENS = 16
 
@@ -27,7 +30,7 @@ HASH_BLOCK_TOKENS = 16
 EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
            "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
            "kv_store_gather", "kv_group_jobs_by_slot", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
-           "kv_host_device_pointer", "kv_version"]
+           "kv_host_device_pointer", "kv_version", "kv_sim_run"]
 
 
 class KvError(RuntimeError):
@@ -41,6 +44,23 @@ class KvLayout(ct.Structure):
                 ("elem_bytes", ct.c_int32), ("block_size", ct.c_int32), ("chunk_tokens", ct.c_int32),
                 ("num_blocks", ct.c_int64), ("num_slots", ct.c_int64), ("paged_kv_stride", ct.c_int64),
                 ("paged_block_stride", ct.c_int64)]
+
+
+class KvSimConfig(ct.Structure):
+    _fields_ = [("budget_bytes", ct.c_double), ("capacity_bytes", ct.c_double), ("stage_rate", ct.c_double),
+                ("static_rate", ct.c_double), ("gpu_rate", ct.c_double), ("prefill_s", ct.c_double),
+                ("decode_s", ct.c_double), ("tick_s", ct.c_double), ("max_active", ct.c_int32),
+                ("policy", ct.c_int32), ("queue_k", ct.c_int32), ("reserved", ct.c_int32)]
+
+
+class KvSimResult(ct.Structure):
+    _fields_ = [("area_byte_s", ct.c_double), ("cost_gib_s_per_request", ct.c_double), ("end_s", ct.c_double),
+                ("p_max_bytes", ct.c_double), ("committed", ct.c_int32), ("blocked", ct.c_int32),
+                ("ordinary", ct.c_int32), ("reserved", ct.c_int32), ("events", ct.c_int64)]
+
+
+class KvSimEvent(ct.Structure):
+    _fields_ = [("t", ct.c_double), ("kind", ct.c_int32), ("id", ct.c_int32)]
 
 
 _lib: Optional[ct.CDLL] = None
@@ -78,6 +98,8 @@ def lib() -> ct.CDLL:
         "kv_strerror": [ct.c_int],
         "kv_host_device_pointer": [_vp, ct.POINTER(_vp)],
         "kv_version": [],
+        "kv_sim_run": [ct.POINTER(KvSimConfig), _vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp,
+                       ct.POINTER(KvSimResult), _vp, _i64, ct.POINTER(_i64)],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -321,3 +343,37 @@ def kv_host_device_pointer(host_ptr: int) -> int:
     d = _vp()
     _check(lib().kv_host_device_pointer(host_ptr, ct.byref(d)), "kv_host_device_pointer")
     return d.value
+
+
+def kv_sim_run(config: KvSimConfig, obj_bytes, arrival, manifests, uncached, out_tokens, trace: bool = False):
+    """Run the controller simulation.  Returns (result, first_token, done,
+    trace) where trace is a list of (t, kind name, id) if requested."""
+    ob = np.ascontiguousarray(obj_bytes, np.float64)
+    arr = np.ascontiguousarray(arrival, np.float64)
+    N = arr.size
+    off = np.zeros(N + 1, np.int64)
+    np.cumsum([len(m) for m in manifests], out=off[1:])
+    objs = np.ascontiguousarray(np.concatenate([np.asarray(m, np.int32) for m in manifests]) if N and off[-1]
+                                else np.zeros(1, np.int32), np.int32)
+    unc = np.ascontiguousarray(uncached, np.int32)
+    out = np.ascontiguousarray(out_tokens, np.int32)
+    ft = np.zeros(max(N, 1), np.float64)
+    dn = np.zeros(max(N, 1), np.float64)
+    res = KvSimResult()
+    n_tr = _i64(0)
+    buf = None
+    cap = 0
+    if trace:
+        cap = 64 * (N + ob.size) + 1024
+        buf = (KvSimEvent * cap)()
+    rc = lib().kv_sim_run(ct.byref(config), ob.ctypes.data if ob.size else None, ob.size, arr.ctypes.data,
+                          off.ctypes.data, objs.ctypes.data, unc.ctypes.data, out.ctypes.data, N, ft.ctypes.data,
+                          dn.ctypes.data, ct.byref(res), ct.cast(buf, ct.c_void_p) if buf is not None else None,
+                          cap, ct.byref(n_tr))
+    _check(rc, "kv_sim_run")
+    events = None
+    if trace:
+        if n_tr.value > cap:
+            raise RuntimeError("trace buffer too small")
+        events = [(buf[k].t, SIM_TRACE_KINDS[buf[k].kind], buf[k].id) for k in range(n_tr.value)]
+    return res, ft[:N].copy(), dn[:N].copy(), events

@@ -517,3 +517,59 @@ CONFIGS = {
 
 def make(name: str) -> Workload:
     return CONFIGS[name]()
+
+
+# --------------------------------------------------------------------------
+# Controller scenarios (request streams for the commitment simulator)
+# --------------------------------------------------------------------------
+
+@dataclass
+class StagingScenario:
+    """Inputs of one controller simulation: staged objects and a request stream."""
+    name: str
+    obj_bytes: List[float]
+    arrival: List[float]
+    manifests: List[List[int]]
+    uncached: List[int]
+    out_tokens: List[int]
+
+
+def policy_scenario(ratio: float, seed: int = 7, kv_bytes_per_token: int = 128 * 1024, chunk: int = 256,
+                    gap_s: float = 0.5, out_tokens: int = 128, question_tokens: int = 32) -> StagingScenario:
+    """Shaped like the paper's policy experiment (Section 5): 12 documents, four
+    from each of three length groups spanning 16,078-67,744 tokens (lengths
+    drawn uniformly inside each group, no dataset text), one request per
+    document in a fixed random order every ``gap_s`` seconds; the prefix
+    ``ratio`` of each document is retained as complete 256-token chunks (each
+    an object of chunk x KV bytes per token); the rest of the document plus a
+    question is prefilled; ``out_tokens`` are generated."""
+    rng = _rng(seed, _P_LEN)
+    groups = [(16078, 30000), (30000, 48000), (48000, 67744)]
+    lengths = [int(rng.integers(lo, hi + 1)) for lo, hi in groups for _ in range(4)]
+    order = _rng(seed, _P_PERM).permutation(len(lengths))
+    obj, man, unc, arr = [], [], [], []
+    for k, d in enumerate(order):
+        n = lengths[d]
+        kept = int(math.floor(ratio * n / chunk))
+        ids = list(range(len(obj), len(obj) + kept))
+        obj += [float(chunk * kv_bytes_per_token)] * kept
+        man.append(ids)
+        unc.append(n - kept * chunk + question_tokens)
+        arr.append(gap_s * k)
+    return StagingScenario(f"policy-12docs-p{int(ratio * 100)}", obj, arr, man, unc, [out_tokens] * len(man))
+
+
+def shared_prefix_scenario(n: int, seed: int = 11, n_prefixes: int = 64, chunks_max: int = 64,
+                           chunk_bytes: int = 32 << 20, gap_s: float = 0.05) -> StagingScenario:
+    """A long request stream for timing the simulator: ``n`` requests drawing
+    Zipf(1.1) over ``n_prefixes`` shared prefixes, each request reusing a
+    random number of its prefix's chunks."""
+    rng = _rng(seed, _P_ZIPF)
+    pid = rng.choice(n_prefixes, size=n, p=_zipf_probs(n_prefixes, 1.1))
+    lens = _rng(seed, _P_LEN).integers(1, chunks_max + 1, size=n_prefixes)
+    base = np.concatenate([[0], np.cumsum(lens)]).astype(int)
+    use = _rng(seed, _P_SMALL).integers(0, chunks_max + 1, size=n)
+    man = [list(range(base[p], base[p] + min(int(u), int(lens[p])))) for p, u in zip(pid, use)]
+    unc = [int(x) for x in _rng(seed, _P_TOK).integers(100, 4000, size=n)]
+    return StagingScenario(f"shared-{n}", [float(chunk_bytes)] * int(base[-1]), [gap_s * i for i in range(n)], man,
+                           unc, [64] * n)
