@@ -228,6 +228,13 @@ def main() -> int:
                     help="run the claim/commitment controller simulation (host only) and exit")
     ap.add_argument("--calib-copy", action="store_true",
                     help="only run a plain 4 GiB contiguous copy (counter calibration) and exit")
+    ap.add_argument("--lower-tier", default="zero-copy", choices=("zero-copy", "pipelined", "serialized"),
+                    help="workloads whose staged chunks live in host memory: read them in place (zero-copy), or "
+                         "stage them into HBM by DMA batch by batch, overlapped with the scatter on a second "
+                         "stream (pipelined) or on the same stream (serialized); staged modes start every step "
+                         "with no chunk resident in HBM")
+    ap.add_argument("--slots-per-batch", type=int, default=4,
+                    help="staged modes: distinct staged chunks per copy/scatter batch")
     ap.add_argument("--no-fill", action="store_true",
                     help="leave KV buffers uninitialised (hardware-counter runs: no generator kernels run; the "
                          "copies move the same bytes) and skip the device-copy and CPU-baseline extras")
@@ -259,11 +266,12 @@ def main() -> int:
     w = W.make(args.workload)
     print(f"[bench] workload {w.name}: {w.num_reqs} requests, pool {w.pool_bytes() / 2**30:.1f} GiB, "
           f"staging {w.staged_bytes() / 2**30:.1f} GiB", file=sys.stderr, flush=True)
-    path = StagingPath(w)
+    path = StagingPath(w, lower_tier=args.lower_tier, slots_per_batch=args.slots_per_batch)
     if not args.no_fill:
         path.fill(STG_TAG, POOL_TAG, w.seed)
     path.prestage()
     for _ in range(args.warmup):
+        path.drop_fast_tier()
         path.run_pass(evict_stored=True)
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
@@ -272,6 +280,7 @@ def main() -> int:
     t0 = time.perf_counter()
     stats = None
     for _ in range(args.steps):
+        path.drop_fast_tier()          # staged modes: every step stages its chunks again
         stats = path.run_pass(evict_stored=True, timers=timers)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -285,7 +294,7 @@ def main() -> int:
     r_bytes = 2 * stats.retrieve_bytes          # read + write per step
     s_bytes = 2 * stats.store_bytes
     value = (r_bytes + s_bytes) / (ms_step * 1e-3) / 1e9
-    k_ms = {k: avg_ms(k) for k in ("hash", "lookup", "retrieve", "store")}
+    k_ms = {k: avg_ms(k) for k in ("hash", "lookup", "retrieve", "store", "stage")}
     r_gbs = r_bytes / (k_ms["retrieve"] * 1e-3) / 1e9 if k_ms["retrieve"] else 0.0
     s_gbs = s_bytes / (k_ms["store"] * 1e-3) / 1e9 if k_ms["store"] else 0.0
     n_tok = int(w.tokens.size)
@@ -329,6 +338,15 @@ def main() -> int:
         },
         "source_digest": _src_digest(),
     }
+    if w.staging_in_host:
+        lt = {"mode": args.lower_tier, "staged_bytes_per_step": stats.staged_bytes}
+        if path.staged_mode:
+            lt["slots_per_batch"] = args.slots_per_batch
+            lt["retrieve_ms_includes_staging"] = True
+            if k_ms["stage"]:
+                lt["stage_ms"] = round(k_ms["stage"], 4)
+                lt["stage_GB/s"] = round(stats.staged_bytes / (k_ms["stage"] * 1e-3) / 1e9, 1)
+        line["config"]["lower_tier"] = lt
     del path
     torch.cuda.synchronize()
     torch.cuda.empty_cache()

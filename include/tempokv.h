@@ -13,6 +13,10 @@
  *   kv_retrieve_scatter   staged chunk [L,2,C,H,D] -> paged KV blocks (one launch)
  *   kv_store_gather       paged KV blocks -> staged chunk (one launch)
  *   kv_commit_should_stage  the TTU/TTR commitment rule of Section 3.2 (host)
+ *   kv_stage_in / kv_retrieve_pipelined  lower tier -> HBM staging, and the
+ *                         retrieve gated on those copies (stage-ready)
+ *   kv_sim_run            claim/commitment controller in a discrete-event
+ *                         simulation (Sections 3.1-3.3)
  *
  * Conventions shared by every call
  * --------------------------------
@@ -210,6 +214,63 @@ int kv_store_gather(const kv_layout *layout, void *d_staging, const void *const 
  * call); the retrieve kernel reads a staged chunk once per unit when the
  * jobs sharing it run back to back.  Errors: KV_EINVAL. */
 int kv_group_jobs_by_slot(kv_job *h_jobs, int32_t num_jobs);
+
+/* ----------------------------------------------------------------------- */
+/* Staging into HBM and the stage-ready-gated retrieve                      */
+/* ----------------------------------------------------------------------- */
+
+/* The paper separates staging (SSD -> fast tier) from retrieval (fast tier ->
+ * GPU), and calls the matched KV stage-ready once every object it needs is
+ * present in the fast tier and protected (Section 2.2).  Here pinned host
+ * memory stands in for the lower tier and the HBM staging buffer is the fast
+ * tier: h_lower_tier holds slots in the same [S][L][2][C][H][D] layout, slot
+ * s at byte s*slot_bytes of both buffers.  h_lower_tier should come from
+ * hipHostMalloc (pageable memory also works, but its copies do not overlap). */
+
+/* Stage slots h_slots[0..n) of the lower tier into the same slots of
+ * d_staging: DMA copies (hipMemcpyAsync) on `stream`, one per run of
+ * consecutive slot ids.  Every slot is checked before anything is enqueued.
+ * Errors: KV_EINVAL, KV_ERANGE (slot outside [0, num_slots)), KV_EHIP. */
+int kv_stage_in(const kv_layout *layout, const void *h_lower_tier, void *d_staging, const int32_t *h_slots,
+                int32_t n, void *stream);
+
+/* The reverse copy, fast tier -> lower tier, for the same slots (retaining
+ * stored chunks below the fast tier).  Same checks and errors. */
+int kv_stage_out(const kv_layout *layout, const void *d_staging, void *h_lower_tier, const int32_t *h_slots,
+                 int32_t n, void *stream);
+
+/* Events for kv_retrieve_pipelined (one per batch, up to max_batches batches
+ * per call), created on the current device; the caller owns the object and
+ * frees it with kv_pipeline_destroy, which first waits for its events.  One
+ * object serves one call at a time; calls that overlap on two host threads
+ * race.  Errors: KV_EINVAL, KV_EHIP. */
+typedef struct kv_pipeline kv_pipeline;
+int kv_pipeline_create(int32_t max_batches, kv_pipeline **out);
+int kv_pipeline_destroy(kv_pipeline *pl);
+
+/* Retrieve whose staged chunks start in the lower tier.  The jobs should be
+ * grouped by slot (kv_group_jobs_by_slot); h_jobs is their host copy, d_jobs
+ * the same array on the device.  They are cut into batches of
+ * `slots_per_batch` distinct slots (raised if needed so that at most the
+ * pipeline's max_batches batches are formed).  For each batch its slots are
+ * staged on copy_stream, an event recorded after those copies marks them
+ * stage-ready, and `stream` waits for that event before the retrieve scatter
+ * of the batch's jobs: retrieval of a chunk begins only once it is
+ * stage-ready (Sections 2.2 and 3.2), and the copy of the next batch overlaps
+ * the scatter of this one.  Afterwards the staged slots are also resident in
+ * d_staging.  Passing one stream as both copy_stream and stream serialises
+ * every copy with its scatter.  Ungrouped jobs give the same result, but a
+ * slot is then staged once per batch that names it.  The copies are not
+ * ordered after earlier work on `stream`: the caller makes copy_stream wait
+ * for any such work that still reads or writes the staged slots.  Every
+ * argument and job slot is checked before anything is enqueued; a KV_EHIP
+ * part-way leaves the batches before it enqueued.  Errors: those of
+ * kv_retrieve_scatter and kv_stage_in, and KV_EINVAL when the current device
+ * is not the pipeline's. */
+int kv_retrieve_pipelined(kv_pipeline *pl, const kv_layout *layout, const void *h_lower_tier, void *d_staging,
+                          void *const *h_layer_ptrs, const int32_t *d_block_tables, int32_t bt_stride,
+                          int32_t num_reqs, const kv_job *h_jobs, const kv_job *d_jobs, int32_t num_jobs,
+                          int32_t slots_per_batch, void *copy_stream, void *stream);
 
 /* Host check of a job batch against copies of its tables: KV_ERANGE if any
  * slot, request, chunk or (valid-job) block id is out of range or any

@@ -30,7 +30,8 @@ HASH_BLOCK_TOKENS = 16
 EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
            "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
            "kv_store_gather", "kv_group_jobs_by_slot", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
-           "kv_host_device_pointer", "kv_version", "kv_sim_run"]
+           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out", "kv_pipeline_create",
+           "kv_pipeline_destroy", "kv_retrieve_pipelined"]
 
 
 class KvError(RuntimeError):
@@ -100,6 +101,12 @@ def lib() -> ct.CDLL:
         "kv_version": [],
         "kv_sim_run": [ct.POINTER(KvSimConfig), _vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp,
                        ct.POINTER(KvSimResult), _vp, _i64, ct.POINTER(_i64)],
+        "kv_stage_in": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _vp],
+        "kv_stage_out": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _vp],
+        "kv_pipeline_create": [_i32, ct.POINTER(_vp)],
+        "kv_pipeline_destroy": [_vp],
+        "kv_retrieve_pipelined": [_vp, ct.POINTER(KvLayout), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _i32, _i32,
+                                  _vp, _vp],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -312,6 +319,83 @@ def kv_store_gather(layout: KvLayout, d_staging, layers: Sequence, d_block_table
                                  _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
                                  _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
                                  _stream(stream)), "kv_store_gather")
+
+
+def _hptr(t, what: str = "host buffer") -> int:
+    """Address of a pinned host tensor (torch, pin_memory) or an int address."""
+    if isinstance(t, int):
+        return t
+    if t.is_cuda:
+        raise ValueError(f"{what} must be in host memory")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if not t.is_pinned():
+        raise ValueError(f"{what} must be pinned (asynchronous DMA copies need page-locked memory)")
+    return t.data_ptr()
+
+
+def kv_stage_in(layout: KvLayout, h_lower_tier, d_staging, slots, stream=None) -> None:
+    """DMA copies of the listed slots, lower tier (pinned host) -> HBM staging."""
+    sl = np.ascontiguousarray(slots, np.int32).reshape(-1)
+    _check(lib().kv_stage_in(ct.byref(layout), _hptr(h_lower_tier, "lower tier") if sl.size else None,
+                             _dptr(d_staging, None, "staging") if sl.size else None,
+                             sl.ctypes.data if sl.size else None, sl.size, _stream(stream)), "kv_stage_in")
+
+
+def kv_stage_out(layout: KvLayout, d_staging, h_lower_tier, slots, stream=None) -> None:
+    """DMA copies of the listed slots, HBM staging -> lower tier (pinned host)."""
+    sl = np.ascontiguousarray(slots, np.int32).reshape(-1)
+    _check(lib().kv_stage_out(ct.byref(layout), _dptr(d_staging, None, "staging") if sl.size else None,
+                              _hptr(h_lower_tier, "lower tier") if sl.size else None,
+                              sl.ctypes.data if sl.size else None, sl.size, _stream(stream)), "kv_stage_out")
+
+
+class KvPipeline:
+    """Owner of the events of kv_retrieve_pipelined (kv_pipeline_create)."""
+
+    def __init__(self, max_batches: int = 64):
+        h = _vp()
+        _check(lib().kv_pipeline_create(max_batches, ct.byref(h)), "kv_pipeline_create")
+        self.handle = h.value
+        self.max_batches = max_batches
+
+    def close(self) -> None:
+        if self.handle:
+            _check(lib().kv_pipeline_destroy(self.handle), "kv_pipeline_destroy")
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def kv_retrieve_pipelined(pipeline: KvPipeline, layout: KvLayout, h_lower_tier, d_staging, layers: Sequence,
+                          d_block_tables, bt_stride: int, num_reqs: int, h_jobs: np.ndarray, d_jobs,
+                          slots_per_batch: int, copy_stream, stream=None) -> None:
+    """Retrieve whose chunks start in the lower tier: per batch of slots,
+    DMA copy on copy_stream, then the scatter on `stream` once they landed.
+    h_jobs ([n,4] int32, grouped by slot) and d_jobs hold the same jobs."""
+    import torch
+    if len(layers) != layout.num_layers:
+        raise ValueError("one paged tensor per layer is required")
+    hj = np.ascontiguousarray(h_jobs, np.int32).reshape(-1, 4)
+    n = hj.shape[0]
+    if n and (d_jobs is None or int(d_jobs.numel()) != 4 * n):
+        raise ValueError("d_jobs must hold the same jobs as h_jobs")
+    _check(lib().kv_retrieve_pipelined(pipeline.handle, ct.byref(layout), _hptr(h_lower_tier, "lower tier") if n else None,
+                                       _dptr(d_staging, None, "staging"), _layer_array(layers),
+                                       _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
+                                       hj.ctypes.data if n else None,
+                                       _dptr(d_jobs, torch.int32, "jobs") if n else None, n, slots_per_batch,
+                                       _stream(copy_stream), _stream(stream)), "kv_retrieve_pipelined")
 
 
 def kv_group_jobs_by_slot(jobs: np.ndarray) -> np.ndarray:

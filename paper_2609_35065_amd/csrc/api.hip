@@ -14,8 +14,10 @@ namespace {
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
-// Layout checks shared by the two copy directions.
-int check_layout(const kv_layout *lo) {
+}  // namespace
+
+// Layout checks shared by the copy directions and staging.
+int tkv::check_layout(const kv_layout *lo) {
     if (!lo) return KV_EINVAL;
     if (lo->num_layers <= 0 || lo->num_layers > KV_MAX_LAYERS || lo->kv_heads <= 0 || lo->head_dim <= 0 ||
         lo->block_size <= 0 || lo->chunk_tokens <= 0 || lo->num_blocks <= 0 || lo->num_slots <= 0)
@@ -33,6 +35,12 @@ int check_layout(const kv_layout *lo) {
     return KV_OK;
 }
 
+namespace {
+using tkv::check_layout;
+
+}  // namespace
+
+namespace tkv {
 int make_copy_params(tkv::CopyParams &p, const kv_layout *lo, const void *staging, const void *const *layers,
                      const int32_t *bt, int32_t bt_stride, int32_t num_reqs, const kv_job *jobs,
                      int32_t num_jobs) {
@@ -65,7 +73,10 @@ int make_copy_params(tkv::CopyParams &p, const kv_layout *lo, const void *stagin
     p.total_segs = (int64_t)num_jobs * lo->num_layers * 2 * nseg;
     return KV_OK;
 }
+}  // namespace tkv
 
+namespace {
+using tkv::make_copy_params;
 }  // namespace
 
 extern "C" {

@@ -56,7 +56,13 @@ hipError_t launch_lookup(const IndexEntry *table, int log2cap, const uint64_t *b
                          const int64_t *blk_off, int32_t num_reqs, int32_t bpc, const int64_t *chunk_off,
                          int32_t *chunk_slot, int32_t *hit_chunks, hipStream_t stream);
 
-// Device table of an index, for kv_lookup (index.cpp).
+// Argument checks and launch parameters shared by the copy entry points
+// (api.hip).  Return KV_OK or a negative kv_status.
+int check_layout(const kv_layout *lo);
+int make_copy_params(CopyParams &p, const kv_layout *lo, const void *staging, const void *const *layers,
+                     const int32_t *bt, int32_t bt_stride, int32_t num_reqs, const kv_job *jobs, int32_t num_jobs);
+
+// Device table of an index, for kv_lookup (index.hip).
 const IndexEntry *index_device_table(const kv_index *idx, int *log2cap);
 
 }  // namespace tkv

@@ -8,6 +8,18 @@ index update (kv_index_insert; optionally kv_index_erase of what was just
 stored, which returns the batch to its starting state so that passes can be
 repeated).
 
+When the workload keeps its staged chunks in host memory, ``lower_tier``
+picks how the retrieve reaches them:
+  "zero-copy"   the scatter reads the pinned host buffer through its device
+                mapping (kv_retrieve_scatter on a host-mapped pointer);
+  "pipelined"   host memory is the lower tier and an HBM staging buffer the
+                fast tier: chunks not resident in HBM are staged by DMA on a
+                second stream, batch by batch, and each batch's scatter waits
+                for its copies (kv_retrieve_pipelined);
+  "serialized"  the same, with copies and scatters on one stream.
+In the two staged modes the store gathers into the HBM staging buffer and
+copies the stored slots back to host memory (kv_stage_out).
+
 This module only sequences the C calls and owns the buffers they read and
 write; it computes nothing itself.
 """
@@ -19,8 +31,11 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, kv_build_jobs, kv_commit_should_stage, kv_group_jobs_by_slot,
-               kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_scatter, kv_store_gather, make_layout)
+from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, KvPipeline, kv_build_jobs, kv_commit_should_stage,
+               kv_group_jobs_by_slot, kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_pipelined,
+               kv_retrieve_scatter, kv_stage_out, kv_store_gather, make_layout)
+
+LOWER_TIER_MODES = ("zero-copy", "pipelined", "serialized")
 
 
 @dataclass
@@ -30,6 +45,7 @@ class PassStats:
     dropped: int = 0
     retrieve_bytes: int = 0      # payload copied by the scatter (read = written)
     store_bytes: int = 0
+    staged_bytes: int = 0        # lower tier -> HBM by DMA (staged modes)
     commits: int = 0
     decisions: Dict[int, int] = field(default_factory=dict)
 
@@ -43,7 +59,10 @@ class StagingPath:
     provides shapes, token ids, block tables and which chunks are staged at
     the start.  KV contents are filled by the caller (see ``fill``)."""
 
-    def __init__(self, w, device: str = "cuda", hash_seed: int = 0, stream: Optional[torch.cuda.Stream] = None):
+    def __init__(self, w, device: str = "cuda", hash_seed: int = 0, stream: Optional[torch.cuda.Stream] = None,
+                 lower_tier: str = "zero-copy", slots_per_batch: int = 4):
+        if lower_tier not in LOWER_TIER_MODES:
+            raise ValueError(f"lower_tier must be one of {LOWER_TIER_MODES}")
         self.w = w
         self.dev = torch.device(device)
         self.hash_seed = hash_seed
@@ -54,16 +73,25 @@ class StagingPath:
                                             s.chunk_tokens, w.num_blocks, w.num_slots, kv_stride, block_stride)
         self.bpc = s.chunk_tokens // 16
         d = self.dev
+        self.staged_mode = w.staging_in_host and lower_tier != "zero-copy"
+        self.slots_per_batch = slots_per_batch
+        self.resident = np.zeros(w.num_slots, bool)   # slots whose HBM copy is current (staged modes)
         with torch.cuda.stream(self.stream):
             self.staging_host = None
             if w.staging_in_host:
                 self.staging_host = torch.empty(w.staged_bytes(), dtype=torch.uint8, pin_memory=True)
                 self.staging_ptr = kv_host_device_pointer(self.staging_host.data_ptr())
                 self.staging = None
+                if self.staged_mode:
+                    self.staging = torch.empty(w.staged_bytes(), dtype=torch.uint8, device=d)
+                    self.staging_ptr = self.staging.data_ptr()
             else:
                 self.staging = torch.empty(w.staged_bytes(), dtype=torch.uint8, device=d)
                 self.staging_ptr = self.staging.data_ptr()
             self.layers = [torch.empty(w.layer_bytes(), dtype=torch.uint8, device=d) for _ in range(s.num_layers)]
+        if self.staged_mode:
+            self.copy_stream = (torch.cuda.Stream(self.dev) if lower_tier == "pipelined" else self.stream)
+            self.pipeline = KvPipeline(64)
         self.set_batch(w)
         self.index = KvIndex(max(w.num_slots, 1))
         self.free: List[int] = []
@@ -103,14 +131,22 @@ class StagingPath:
 
     # ------------------------------------------------------------------
     def staging_view(self) -> torch.Tensor:
-        return self.staging_host if self.staging is None else self.staging
+        """The authoritative staged chunks: the host buffer when the workload
+        keeps them in host memory, else the HBM staging buffer."""
+        return self.staging_host if self.staging_host is not None else self.staging
+
+    def drop_fast_tier(self) -> None:
+        """Forget which slots are resident in HBM (staged modes): the next
+        retrieve stages every chunk it reads from host memory again."""
+        self.resident[:] = False
 
     def fill(self, staging_tag: int, pool_tag_base: int, seed: int, finite: bool = True) -> None:
         """Fill staging and pool with the workload KV formula (input generation).
         Layer l of the pool uses tag ``pool_tag_base + l``."""
         from workloads import fill_kv_
+        self.resident[:] = False
         with torch.cuda.stream(self.stream):
-            if self.staging is not None:
+            if self.staging_host is None:
                 fill_kv_(self.staging, staging_tag, seed, finite)
             else:
                 # host staging: fill device windows and copy them into the pinned buffer
@@ -194,21 +230,45 @@ class StagingPath:
             assert kv_validate_jobs(self.layout, w.block_tables, retr, False) == 0 or len(retr) == 0
             assert kv_validate_jobs(self.layout, w.block_tables, store, True) == 0 or len(store) == 0
         nr, ns = len(retr), len(store)
+        nres = nr   # jobs whose chunk is already in the staging buffer the scatter reads
         with torch.cuda.stream(self.stream):
             if nr:
                 # jobs sharing a staged chunk run back to back (results do not depend on order)
-                self.h_retr.numpy()[:nr] = kv_group_jobs_by_slot(retr)
+                grouped = kv_group_jobs_by_slot(retr)
+                if self.staged_mode:
+                    # resident chunks first (plain scatter), then the ones to stage
+                    here = self.resident[grouped[:, 0]]
+                    grouped = np.concatenate([grouped[here], grouped[~here]])
+                    nres = int(here.sum())
+                self.h_retr.numpy()[:nr] = grouped
                 self.d_retr[:nr].copy_(self.h_retr[:nr], non_blocking=True)
             if ns:
                 self.h_store.numpy()[:ns] = store
                 self.d_store[:ns].copy_(self.h_store[:ns], non_blocking=True)
             e = self._ev(timers, "retrieve")
-            kv_retrieve_scatter(self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_retr, nr,
-                                self.stream)
+            kv_retrieve_scatter(self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_retr,
+                                nres, self.stream)
+            if nres < nr:
+                h_jobs = self.h_retr.numpy()[nres:nr]
+                es = None
+                if self.copy_stream is not self.stream:
+                    self.copy_stream.wait_stream(self.stream)
+                    es = self._ev(timers, "stage", self.copy_stream)   # the copies alone
+                kv_retrieve_pipelined(self.pipeline, self.layout, self.staging_host, self.staging, self.layers,
+                                      self.bt, w.bt_stride, R, h_jobs, self.d_retr[nres:nr], self.slots_per_batch,
+                                      self.copy_stream, self.stream)
+                self._ev_end(es, self.copy_stream)
+                staged = np.unique(h_jobs[:, 0])
+                self.resident[staged] = True
+                st.staged_bytes = int(staged.size) * slot_bytes
             self._ev_end(e)
             e = self._ev(timers, "store")
             kv_store_gather(self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_store, ns,
                             self.stream)
+            if self.staged_mode and ns:
+                # retain the stored chunks in host memory too; their HBM copy is current
+                kv_stage_out(self.layout, self.staging, self.staging_host, np.sort(store[:, 0]), self.stream)
+                self.resident[store[:, 0]] = True
             self._ev_end(e)
             if ns:
                 self.index.insert(skeys, store[:, 0].copy(), self.stream)
@@ -220,17 +280,17 @@ class StagingPath:
             self.evict_last()
         return st
 
-    def _ev(self, timers, name):
+    def _ev(self, timers, name, stream=None):
         if timers is None:
             return None
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(self.stream)
+        a.record(stream if stream is not None else self.stream)
         timers.setdefault(name, []).append((a, b))
         return b
 
-    def _ev_end(self, b) -> None:
+    def _ev_end(self, b, stream=None) -> None:
         if b is not None:
-            b.record(self.stream)
+            b.record(stream if stream is not None else self.stream)
 
     def evict_last(self) -> None:
         """Erase the keys stored by the last pass and free their slots."""

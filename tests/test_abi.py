@@ -175,3 +175,37 @@ def test_group_jobs_by_slot_is_a_stable_sort(seed):
     want = jobs[np.argsort(jobs[:, 0], kind="stable")]
     assert np.array_equal(got, want)
     assert kv.lib().kv_group_jobs_by_slot(None, -1) == kv.KV_EINVAL
+
+
+def test_stage_calls_check_arguments_before_any_copy():
+    lo = _layout()
+    L = kv.lib()
+    sl = np.array([0, 1, 3], np.int32)
+    for f in (L.kv_stage_in, L.kv_stage_out):
+        assert f(ct.byref(lo), 0x10000, 0x20000, None, 0, None) == kv.KV_OK            # nothing to copy
+        assert f(ct.byref(lo), 0x10000, 0x20000, sl.ctypes.data, -1, None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), None, 0x20000, sl.ctypes.data, 3, None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), 0x10000, None, sl.ctypes.data, 3, None) == kv.KV_EINVAL
+        assert f(ct.byref(lo), 0x10000, 0x20000, None, 3, None) == kv.KV_EINVAL
+        assert f(None, 0x10000, 0x20000, sl.ctypes.data, 3, None) == kv.KV_EINVAL
+        bad = _layout(num_layers=0)
+        assert f(ct.byref(bad), 0x10000, 0x20000, sl.ctypes.data, 3, None) == kv.KV_EINVAL
+        for s in (-1, lo.num_slots):
+            b = np.array([0, s], np.int32)
+            assert f(ct.byref(lo), 0x10000, 0x20000, b.ctypes.data, 2, None) == kv.KV_ERANGE
+
+
+def test_pipeline_calls_check_arguments():
+    L = kv.lib()
+    h = ct.c_void_p()
+    assert L.kv_pipeline_create(0, ct.byref(h)) == kv.KV_EINVAL
+    assert L.kv_pipeline_create(-3, ct.byref(h)) == kv.KV_EINVAL
+    assert L.kv_pipeline_create(4, None) == kv.KV_EINVAL
+    assert L.kv_pipeline_destroy(None) == kv.KV_EINVAL
+    lo = _layout()
+    layers = (ct.c_void_p * 2)(0x10000, 0x20000)
+    jobs = np.zeros((1, 4), np.int32)
+    assert L.kv_retrieve_pipelined(None, ct.byref(lo), 0x10000, 0x10000, layers, 0x10000, 10, 2, jobs.ctypes.data,
+                                   0x10000, 1, 1, None, None) == kv.KV_EINVAL
+    assert L.kv_retrieve_pipelined(0x1000, ct.byref(lo), 0x10000, 0x10000, layers, 0x10000, 10, 2,
+                                   jobs.ctypes.data, 0x10000, 1, 0, None, None) == kv.KV_EINVAL

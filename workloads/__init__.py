@@ -37,7 +37,7 @@ M32 = 0xFFFFFFFF
 FINITE_MASK = 0xBFFFBFFF   # clears bit 14 of each 16-bit half: no Inf/NaN in fp16 or bf16
 
 # purposes for numpy sub-seeds
-_P_TOK, _P_LEN, _P_ZIPF, _P_PERM, _P_PERM2, _P_SMALL = range(6)
+_P_TOK, _P_LEN, _P_ZIPF, _P_PERM, _P_PERM2, _P_SMALL, _P_JOBS = range(7)
 
 
 # --------------------------------------------------------------------------
@@ -361,6 +361,22 @@ def repermute_block_tables(w: Workload, purpose_salt: int = 0) -> None:
         bt[r, :need[r]] = perm[pos:pos + need[r]]
         pos += int(need[r])
     w.block_tables = bt
+
+
+def random_retrieve_jobs(w: Workload, seed: int, slots_used: int) -> np.ndarray:
+    """Retrieve jobs ([n,4] int32, slot/req/chunk/0) for every complete chunk
+    of the batch, each reading a random slot among the first ``slots_used``
+    (slots repeat: many jobs may read one chunk), in random order, so the list
+    is not grouped by slot.  Destinations are distinct (one job per chunk)."""
+    rng = _rng(seed, _P_JOBS)
+    C = w.shape.chunk_tokens
+    rc = [(r, c) for r in range(w.num_reqs) for c in range(int(w.lengths[r]) // C)]
+    jobs = np.zeros((len(rc), 4), np.int32)
+    if rc:
+        jobs[:, 1:3] = np.array(rc, np.int32)
+        jobs[:, 0] = rng.integers(0, min(slots_used, w.num_slots), size=len(rc))
+        jobs = jobs[rng.permutation(len(rc))]
+    return jobs
 
 
 def _prefix_len(ratio: float, n: int, C: int) -> int:
