@@ -30,11 +30,11 @@ def _seg_view(w, layer_tensor, kv, blk):
     return layer_tensor[off:off + seg], off
 
 
-def check_full_size(name, n_samples=600, seed=0):
+def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy"):
     w = W.make(name)
     print(f"[fullsize] {name}: {w.num_reqs} reqs, pool {w.pool_bytes() / 2**30:.1f} GiB, "
-          f"staging {w.staged_bytes() / 2**30:.1f} GiB", flush=True)
-    g = StagingPath(w)
+          f"staging {w.staged_bytes() / 2**30:.1f} GiB, lower tier {lower_tier}", flush=True)
+    g = StagingPath(w, lower_tier=lower_tier)
     g.fill(STG_TAG, POOL_TAG, w.seed)
     g.prestage()
     o = OraclePath(w, with_kv=False)
@@ -84,6 +84,13 @@ def check_full_size(name, n_samples=600, seed=0):
         assert np.array_equal(got, exp), (name, "scatter", l, kvp, blk)
     if len(retr):
         assert n_touched > 0
+    # padded block strides: the bytes between segments keep their original contents
+    if w.block_pad:
+        for blk in list(touched[:200]) + [int(b) for b in rng.integers(0, w.num_blocks, 50)]:
+            l, kvp = int(rng.integers(0, L)), int(rng.integers(0, 2))
+            _, off = _seg_view(w, g.layers[l], kvp, int(blk))
+            got = g.layers[l][off + seg:off + seg + w.block_pad].cpu().numpy()
+            assert np.array_equal(got, W.kv_bytes_np(POOL_TAG + l, w.seed, off + seg, w.block_pad)), (name, "pad")
     # --- gather: sampled staging segments of the stored slots
     if len(store):
         slots = [int(store[0, 0]), int(store[-1, 0])] + [int(s) for s in rng.choice(store[:, 0], min(40, len(store)))]
@@ -106,9 +113,18 @@ def check_full_size(name, n_samples=600, seed=0):
 
 FULL = ["l32-64x4096", "l32-lognormal-p25", "l32-lognormal-p50", "l32-lognormal-p75", "l80-32x8192",
         "l32-1024x1024-cap100-hbm", "l32-1024x1024-cap50-hbm", "l32-1024x1024-cap25-hbm",
-        "l32-1024x1024-cap25-host"]
+        "l32-1024x1024-cap25-host", "l32-1x65536", "l48-1x65536", "l48-64x4096", "l32-64x4096-block_first",
+        "l32-64x4096-pad4096"]
 
 
 @pytest.mark.parametrize("name", FULL)
 def test_full_size_sampled(name):
     check_full_size(name)
+
+
+@pytest.mark.parametrize("name", ["l32-1x65536-host", "l32-1024x1024-cap100-host"])
+def test_full_size_sampled_pipelined_from_host(name):
+    # the staged chunks start in pinned host memory and reach HBM by DMA,
+    # batch by batch, before each batch's scatter
+    sg, _ = check_full_size(name, lower_tier="pipelined")
+    assert sg.staged_bytes > 0

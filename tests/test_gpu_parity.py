@@ -125,11 +125,13 @@ SHAPES = [W.KVShape(2, 2, 64, 2, 16, 64), W.KVShape(3, 1, 64, 2, 16, 16), W.KVSh
           W.KVShape(4, 8, 64, 2, 32, 512), W.KVShape(2, 1, 128, 2, 16, 16)]
 
 
-@pytest.mark.parametrize("layout", ["kv_first", "block_first"])
+@pytest.mark.parametrize("layout,pad", [("kv_first", 0), ("block_first", 0), ("kv_first", 4096), ("block_first", 48)])
 @pytest.mark.parametrize("si", range(len(SHAPES)))
-def test_random_workloads(si, layout):
+def test_random_workloads(si, layout, pad):
+    # pad: bytes between consecutive paged segments (padded block strides)
     shape = SHAPES[si]
-    w = W.small_random(100 + si, shape, num_reqs=9, max_len=5 * shape.chunk_tokens + 37, paged_layout=layout)
+    w = W.small_random(100 + si, shape, num_reqs=9, max_len=5 * shape.chunk_tokens + 37, paged_layout=layout,
+                       block_pad=pad)
     g, o = _pair(w)
     for p in range(3):       # stores, then hits on what was stored, then an evicting pass
         evict = p == 2

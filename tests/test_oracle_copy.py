@@ -19,13 +19,20 @@ import oracle
 from workloads import KVShape
 
 
+def _split(layout):
+    """'kv_first', 'block_first', or either with '+<pad>' bytes after every segment."""
+    name, _, pad = layout.partition("+")
+    return name, int(pad or 0)
+
+
 def _setup(seed, L, H, D, e, B, C, layout, num_reqs=3, chunks_per_req=3, spare=5, nslots=6):
     rng = np.random.default_rng(seed)
     shape = KVShape(L, H, D, e, B, C)
     nseg = C // B
     nb = num_reqs * chunks_per_req * nseg + spare
-    seg = shape.seg_bytes
-    if layout == "kv_first":
+    name, pad = _split(layout)
+    seg = shape.seg_bytes + pad
+    if name == "kv_first":
         kv_stride, block_stride = nb * seg, seg
     else:
         kv_stride, block_stride = seg, 2 * seg
@@ -38,17 +45,27 @@ def _setup(seed, L, H, D, e, B, C, layout, num_reqs=3, chunks_per_req=3, spare=5
 
 
 def _paged_view(layer, shape, nb, layout):
+    """[2, NB, B, H, D, e] view (writes go through to ``layer``); padding
+    bytes are outside the view."""
     B, H, D, e = shape.block_size, shape.kv_heads, shape.head_dim, shape.elem_bytes
-    if layout == "kv_first":
-        return layer.reshape(2, nb, B, H, D, e)
-    return layer.reshape(nb, 2, B, H, D, e).transpose(1, 0, 2, 3, 4, 5)
+    name, pad = _split(layout)
+    seg = shape.seg_bytes
+    if name == "kv_first":
+        v = layer.reshape(2, nb, seg + pad)[:, :, :seg]
+    else:
+        v = layer.reshape(nb, 2, seg + pad)[:, :, :seg].transpose(1, 0, 2)
+    v = v.reshape(2, nb, B, H, D, e) if pad == 0 and name == "kv_first" else \
+        np.lib.stride_tricks.as_strided(v, (2, nb, B, H, D, e), v.strides[:2] + (H * D * e, D * e, e, 1))
+    assert np.shares_memory(v, layer)
+    return v
 
 
 SHAPES = [(1, 1, 64, 2, 16, 16), (2, 2, 64, 2, 16, 64), (3, 8, 128, 2, 16, 32),
           (2, 1, 128, 4, 32, 128), (1, 2, 64, 1, 32, 32), (2, 8, 64, 2, 16, 256)]
+LAYOUTS = ["kv_first", "block_first", "kv_first+4096", "block_first+48"]
 
 
-@pytest.mark.parametrize("shape_args,layout", list(itertools.product(SHAPES, ["kv_first", "block_first"])))
+@pytest.mark.parametrize("shape_args,layout", list(itertools.product(SHAPES, LAYOUTS)))
 def test_scatter_matches_numpy_indexing(shape_args, layout):
     shape, lo, bt, staging, layers, nb = _setup(11, *shape_args, layout)
     L, C, B = shape.num_layers, shape.chunk_tokens, shape.block_size
@@ -69,7 +86,7 @@ def test_scatter_matches_numpy_indexing(shape_args, layout):
         assert np.array_equal(a, b)
 
 
-@pytest.mark.parametrize("shape_args,layout", list(itertools.product(SHAPES, ["kv_first", "block_first"])))
+@pytest.mark.parametrize("shape_args,layout", list(itertools.product(SHAPES, LAYOUTS)))
 def test_gather_matches_numpy_indexing(shape_args, layout):
     shape, lo, bt, staging, layers, nb = _setup(12, *shape_args, layout)
     L, C, B = shape.num_layers, shape.chunk_tokens, shape.block_size
@@ -105,7 +122,7 @@ def test_block_equals_chunk_identity_table_is_memcpy():
     assert np.array_equal(back, staging)
 
 
-@pytest.mark.parametrize("layout", ["kv_first", "block_first"])
+@pytest.mark.parametrize("layout", LAYOUTS)
 def test_store_then_retrieve_roundtrip_and_sentinels(layout):
     shape, lo, bt, staging, layers, nb = _setup(21, 2, 2, 64, 2, 16, 64, layout, num_reqs=4,
                                                  chunks_per_req=2, spare=7, nslots=8)
@@ -130,6 +147,12 @@ def test_store_then_retrieve_roundtrip_and_sentinels(layout):
         for blk in range(nb):
             if blk not in touched:
                 assert np.all(got[:, blk] == 0xA5)
+        # padding between segments is never written
+        name, pad = _split(layout)
+        if pad:
+            seg = shape.seg_bytes
+            rows = sentinel[l].reshape(-1, seg + pad)
+            assert np.all(rows[:, seg:] == 0xA5)
 
 
 def test_out_of_range_jobs_and_blocks_touch_nothing():

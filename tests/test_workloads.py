@@ -36,6 +36,34 @@ def test_l32_uniform():
     assert bt.shape == (64, 256) and len(set(bt.ravel().tolist())) == 64 * 256
 
 
+def test_single_prefix_64k():
+    # a 64k-token prefix: 8 GiB of KV at 128 KiB/token, 12 GiB at 192 KiB/token
+    assert W.SHAPE_48L.bytes_per_token == 192 * 1024
+    for name, gib in (("l32-1x65536", 8), ("l48-1x65536", 12), ("l32-1x65536-host", 8)):
+        w = W.make(name)
+        assert w.num_reqs == 1 and w.tokens.size == 65536
+        assert len(w.prestage_chunks) == 256 == w.num_slots
+        assert w.staged_bytes() == gib * 2**30
+        assert np.array_equal(w.tokens, w.prefix_streams[0])
+        assert w.staging_in_host == name.endswith("-host")
+        assert w.num_blocks == 5120 and len(set(w.block_tables.ravel().tolist())) == 4096
+
+
+def test_layout_variants_of_the_64x4096_batch():
+    base = W.make("l32-64x4096")
+    for name, layout, pad in (("l32-64x4096-block_first", "block_first", 0), ("l32-64x4096-pad4096", "kv_first", 4096),
+                              ("l48-64x4096", "kv_first", 0)):
+        w = W.make(name)
+        assert w.paged_layout == layout and w.block_pad == pad
+        assert np.array_equal(w.tokens, base.tokens) and np.array_equal(w.block_tables, base.block_tables)
+        seg = w.shape.seg_bytes + pad
+        kvs, bs = w.strides()
+        assert (kvs, bs) == ((w.num_blocks * seg, seg) if layout == "kv_first" else (seg, 2 * seg))
+        assert w.layer_bytes() == 2 * w.num_blocks * seg
+    assert W.make("l48-64x4096").staged_bytes() == 576 * 48 * 2**20
+    assert W.make("l32-64x4096-pad4096").pool_bytes() == 40 * 2**30 * 36 // 32
+
+
 def test_l80_long():
     w = W.l80_long()
     assert w.num_blocks == 18023 and w.num_slots == 1024

@@ -242,6 +242,7 @@ class Workload:
     block_tables: np.ndarray      # int32 [R, bt_stride], -1 beyond a request's blocks
     staging_in_host: bool = False
     paged_layout: str = "kv_first"    # "kv_first": per layer [2, NB, B, H, D]; "block_first": [NB, 2, B, H, D]
+    block_pad: int = 0            # bytes after each [B, H, D] segment of the paged pool (multiple of 16)
     notes: Dict[str, object] = field(default_factory=dict)
 
     @property
@@ -262,7 +263,7 @@ class Workload:
 
     def strides(self) -> Tuple[int, int]:
         """(kv_stride, block_stride) in bytes within one layer's paged tensor."""
-        seg = self.shape.seg_bytes
+        seg = self.shape.seg_bytes + self.block_pad
         if self.paged_layout == "kv_first":
             return self.num_blocks * seg, seg
         if self.paged_layout == "block_first":
@@ -270,7 +271,7 @@ class Workload:
         raise ValueError(self.paged_layout)
 
     def layer_bytes(self) -> int:
-        return 2 * self.num_blocks * self.shape.seg_bytes
+        return 2 * self.num_blocks * (self.shape.seg_bytes + self.block_pad)
 
     def offsets(self):
         """(blk_off, chunk_off) int64 arrays for the ragged hash / lookup outputs."""
@@ -309,7 +310,7 @@ def _rng(seed: int, purpose: int) -> np.random.Generator:
 
 def _assemble(name, shape, seed, lengths, prefix_id, prefix_tokens, n_prefixes,
               prestage, num_slots, pool_factor, pool_blocks=None, staging_in_host=False,
-              notes=None, paged_layout="kv_first") -> Workload:
+              notes=None, paged_layout="kv_first", block_pad=0) -> Workload:
     """Build tokens, streams and block tables from lengths and prefix choices."""
     rng_tok = _rng(seed, _P_TOK)
     lengths = np.asarray(lengths, np.int64)
@@ -347,7 +348,7 @@ def _assemble(name, shape, seed, lengths, prefix_id, prefix_tokens, n_prefixes,
                     prefix_tokens=np.asarray(prefix_tokens, np.int64),
                     prefix_streams=streams, prestage_chunks=list(prestage), num_slots=num_slots,
                     num_blocks=pool_blocks, block_tables=bt, staging_in_host=staging_in_host,
-                    paged_layout=paged_layout, notes=dict(notes or {}))
+                    paged_layout=paged_layout, block_pad=block_pad, notes=dict(notes or {}))
 
 
 def repermute_block_tables(w: Workload, purpose_salt: int = 0) -> None:
@@ -399,6 +400,9 @@ SHAPE_32L = KVShape(num_layers=32, kv_heads=8, head_dim=128, elem_bytes=2, block
                     chunk_tokens=256, dtype="bf16")
 SHAPE_80L = KVShape(num_layers=80, kv_heads=8, head_dim=128, elem_bytes=2, block_size=16,
                     chunk_tokens=256, dtype="bf16")
+# 48 layers x 8 KV heads x 128 dims, bf16: 192 KiB per token (a 14B-class model)
+SHAPE_48L = KVShape(num_layers=48, kv_heads=8, head_dim=128, elem_bytes=2, block_size=16,
+                    chunk_tokens=256, dtype="bf16")
 
 
 def tiny(seed: int = 1) -> Workload:
@@ -413,20 +417,40 @@ def tiny(seed: int = 1) -> Workload:
                      prestage=[], num_slots=32, pool_factor=1.0)
 
 
-def l32_uniform(seed: int = 2) -> Workload:
+def l32_uniform(seed: int = 2, shape: KVShape = SHAPE_32L, paged_layout: str = "kv_first",
+                block_pad: int = 0) -> Workload:
     """32 layers, 8 KV heads, head_dim 128, bf16 (128 KiB/token); block 16,
     chunk 256; 64 requests x 4096 tokens; 50% prefix ratio from 8 shared
     prefixes (request r uses prefix r mod 8); pool 1.25x live tokens; staging
-    holds the 64 prefix chunks plus 512 free slots for the misses."""
+    holds the 64 prefix chunks plus 512 free slots for the misses.  The same
+    batch is also built with another KV shape, paged layout or padded paged
+    block stride."""
     R, n, P = 64, 4096, 8
-    shape = SHAPE_32L
     k = _prefix_len(0.5, n, shape.chunk_tokens)
     pid = [r % P for r in range(R)]
     nck = k // shape.chunk_tokens
     prestage = [(p, j) for p in range(P) for j in range(nck)]
     misses = R * (n // shape.chunk_tokens - nck)
-    return _assemble("l32h8d128-64x4096-p50", shape, seed, [n] * R, pid, [k] * R, P,
-                     prestage=prestage, num_slots=len(prestage) + misses, pool_factor=1.25)
+    name = f"l{shape.num_layers}h{shape.kv_heads}d{shape.head_dim}-64x4096-p50"
+    if paged_layout != "kv_first":
+        name += "-" + paged_layout
+    if block_pad:
+        name += f"-pad{block_pad}"
+    return _assemble(name, shape, seed, [n] * R, pid, [k] * R, P, prestage=prestage,
+                     num_slots=len(prestage) + misses, pool_factor=1.25, paged_layout=paged_layout,
+                     block_pad=block_pad)
+
+
+def single_prefix(shape: KVShape, n: int = 65536, in_host: bool = False, seed: int = 6) -> Workload:
+    """One request of ``n`` tokens that is entirely a staged prefix: every one
+    of its n/C chunks is resident at start, so the pass retrieves all of them
+    (64k tokens: 8 GiB of KV at 128 KiB/token, 12 GiB at 192 KiB/token) and
+    stores nothing.  Pool 1.25x the request's blocks."""
+    k = _prefix_len(1.0, n, shape.chunk_tokens)
+    nck = k // shape.chunk_tokens
+    name = f"l{shape.num_layers}h{shape.kv_heads}d{shape.head_dim}-1x{n}-p100" + ("-host" if in_host else "")
+    return _assemble(name, shape, seed, [n], [0], [k], 1, prestage=[(0, j) for j in range(nck)],
+                     num_slots=nck, pool_factor=1.25, staging_in_host=in_host)
 
 
 def l32_lognormal(ratio: float, seed: int = 3) -> Workload:
@@ -493,7 +517,7 @@ def l32_capacity(cap: float, in_host: bool, seed: int = 5, ring_slots: int = 64)
 
 def small_random(seed: int, shape: KVShape, num_reqs: int, max_len: int, n_prefixes: int = 2,
                  ratio: float = 0.5, pool_factor: float = 1.5, extra_slots: int = 8,
-                 paged_layout: str = "kv_first", prestage_all: bool = True) -> Workload:
+                 paged_layout: str = "kv_first", prestage_all: bool = True, block_pad: int = 0) -> Workload:
     """Small ragged workload for parity tests: random lengths in [0, max_len]
     (including empty, shorter-than-a-block and ragged tails)."""
     rng = _rng(seed, _P_SMALL)
@@ -512,7 +536,8 @@ def small_random(seed: int, shape: KVShape, num_reqs: int, max_len: int, n_prefi
     misses = int(sum(int(n) // C for n in lengths))
     return _assemble(f"random-s{seed}", shape, seed, lengths, pid, k, n_prefixes,
                      prestage=prestage, num_slots=len(prestage) + misses + extra_slots,
-                     pool_factor=pool_factor, pool_blocks=None, paged_layout=paged_layout)
+                     pool_factor=pool_factor, pool_blocks=None, paged_layout=paged_layout,
+                     block_pad=block_pad)
 
 
 CONFIGS = {
@@ -528,6 +553,12 @@ CONFIGS = {
     "l32-1024x1024-cap100-host": lambda: l32_capacity(1.0, True),
     "l32-1024x1024-cap50-host": lambda: l32_capacity(0.5, True),
     "l32-1024x1024-cap25-host": lambda: l32_capacity(0.25, True),
+    "l32-1x65536": lambda: single_prefix(SHAPE_32L),
+    "l32-1x65536-host": lambda: single_prefix(SHAPE_32L, in_host=True),
+    "l48-1x65536": lambda: single_prefix(SHAPE_48L),
+    "l48-64x4096": lambda: l32_uniform(shape=SHAPE_48L),
+    "l32-64x4096-block_first": lambda: l32_uniform(paged_layout="block_first"),
+    "l32-64x4096-pad4096": lambda: l32_uniform(block_pad=4096),
 }
 
 
