@@ -74,7 +74,8 @@ def _cpu_baseline(shape_name: str):
                     prestage=[(p, j) for p in range(2) for j in range(8)], num_slots=16 + 8 * R, pool_factor=1.25)
     o = OraclePath(w, kv_seed=2)
     o.prestage()
-    moved = 0
+    moved = r_moved = s_moved = 0
+    laps: dict = {}
     # the oracle is single-threaded; pin the process to one core while it runs
     prev = os.sched_getaffinity(0) if hasattr(os, "sched_getaffinity") else None
     if prev:
@@ -82,14 +83,20 @@ def _cpu_baseline(shape_name: str):
     try:
         t0 = time.perf_counter()
         for _ in range(passes):
-            so = o.run_pass(evict_stored=True)
-            moved += 2 * (len(so["retrieve"]) + len(so["store"])) * shape.slot_bytes
+            so = o.run_pass(evict_stored=True, timers=laps)
+            r_moved += 2 * len(so["retrieve"]) * shape.slot_bytes
+            s_moved += 2 * len(so["store"]) * shape.slot_bytes
         dt = time.perf_counter() - t0
     finally:
         if prev:
             os.sched_setaffinity(0, prev)
+    moved = r_moved + s_moved
+    per_op = {"hash_Mtok/s": round(passes * w.tokens.size / laps["hash"] / 1e6, 3),
+              "lookup_and_job_build_ms": round(laps["lookup"] * 1e3 / passes, 3),
+              "retrieve_GB/s": round(r_moved / laps["retrieve"] / 1e9, 4),
+              "store_GB/s": round(s_moved / laps["store"] / 1e9, 4)}
     return {"value": round(moved / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "host_cpu": _cpu_model(), "host_nproc": os.cpu_count(),
+            "per_op": per_op, "host_cpu": _cpu_model(), "host_nproc": os.cpu_count(),
             "sample": (f"{passes} oracle passes (hash, lookup, job build, scatter, gather) over {R} requests x 4096 "
                        f"tokens of the {shape.num_layers}-layer bf16 KV shape, 50% prefix from 2 shared prefixes: "
                        f"{len(so['retrieve'])} retrieve + {len(so['store'])} store jobs per pass, "
@@ -198,6 +205,58 @@ def _controller_bench() -> dict:
     return out
 
 
+def _host_link_gbs(torch, nbytes: int = 1 << 30, reps: int = 3) -> dict:
+    """Host-link context for workloads staged in host memory: a DMA copy of a
+    pinned buffer into HBM, and the library's copy kernel reading the same
+    buffer through its device mapping (the calibration layout of
+    _calibration_copy: contiguous, identity table)."""
+    import numpy as np
+    import paper_2609_35065_amd as kv
+    host = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    host.fill_(3)
+    dev = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    dev.copy_(host, non_blocking=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        dev.copy_(host, non_blocking=True)
+    e.record()
+    torch.cuda.synchronize()
+    dma = nbytes / (s.elapsed_time(e) / reps * 1e-3) / 1e9
+    n, seg = nbytes // (1 << 20), 256 * 8 * 128 * 2
+    lo = kv.make_layout(1, 8, 128, 2, 256, 256, n, n, seg, 2 * seg)
+    bt = torch.from_numpy(np.arange(n, dtype=np.int32).reshape(n, 1)).cuda()
+    jobs = torch.from_numpy(np.stack([np.arange(n), np.arange(n), np.zeros(n), np.zeros(n)], 1)
+                            .astype(np.int32)).cuda()
+    mapped = kv.kv_host_device_pointer(host.data_ptr())
+    kv.kv_retrieve_scatter(lo, mapped, [dev], bt, 1, n, jobs, n)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        kv.kv_retrieve_scatter(lo, mapped, [dev], bt, 1, n, jobs, n)
+    e.record()
+    torch.cuda.synchronize()
+    zc = nbytes / (s.elapsed_time(e) / reps * 1e-3) / 1e9
+    del host, dev
+    torch.cuda.empty_cache()
+    return {"host_to_hbm_dma_GB/s": round(dma, 1), "zero_copy_kernel_read_GB/s": round(zc, 1)}
+
+
+def _clocks():
+    """rocm-smi's clock report, if the tool is available (context only)."""
+    import shutil
+    import subprocess
+    exe = shutil.which("rocm-smi")
+    if not exe:
+        return None
+    try:
+        r = subprocess.run([exe, "--showclocks", "--json"], capture_output=True, text=True, timeout=20)
+        return json.loads(r.stdout) if r.returncode == 0 else None
+    except (OSError, ValueError, subprocess.SubprocessError):
+        return None
+
+
 def _device_copy_gbs(torch, nbytes: int = 4 << 30, reps: int = 5) -> float:
     """Plain device-to-device copy rate (read + write bytes / time): practical-peak context."""
     a = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -290,6 +349,10 @@ def main() -> int:
         ev = timers.get(name, [])
         return float(np.mean([a.elapsed_time(b) for a, b in ev])) if ev else 0.0
 
+    def spread(name):
+        ev = [a.elapsed_time(b) for a, b in timers.get(name, [])]
+        return {"ms_median": round(float(np.median(ev)), 4), "ms_min": round(float(np.min(ev)), 4)} if ev else {}
+
     ms_step = (t1 - t0) * 1e3 / args.steps
     r_bytes = 2 * stats.retrieve_bytes          # read + write per step
     s_bytes = 2 * stats.store_bytes
@@ -336,8 +399,12 @@ def main() -> int:
                             "ns_per_chain_step": round(k_ms["hash"] * 1e6 / max(1, int(w.lengths.max()) // 16), 2)},
             "lookup": {"ms": round(k_ms["lookup"], 4)},
         },
+        "timing": "HIP events on the launch stream around every launch of the timed steps; ms = mean",
         "source_digest": _src_digest(),
     }
+    for name, key in (("retrieve", "retrieve_scatter"), ("store", "store_gather"), ("hash", "hash_prefix"),
+                      ("lookup", "lookup")):
+        line["kernels"][key].update(spread(name))
     if w.staging_in_host:
         lt = {"mode": args.lower_tier, "staged_bytes_per_step": stats.staged_bytes}
         if path.staged_mode:
@@ -353,9 +420,11 @@ def main() -> int:
     if not args.no_fill:
         line["practical_peak"] = {"torch_device_copy_GB/s": round(_device_copy_gbs(torch), 1),
                                   "library_contiguous_copy_GB/s": _calibration_copy(torch)["GB/s_rw"]}
+        if w.staging_in_host:
+            line["practical_peak"].update(_host_link_gbs(torch))
         props = torch.cuda.get_device_properties(0)
         line["gpu"] = {"name": props.name, "compute_units": props.multi_processor_count,
-                       "memory_GiB": round(props.total_memory / 2**30, 1)}
+                       "memory_GiB": round(props.total_memory / 2**30, 1), "clocks": _clocks()}
     if not args.no_cpu_baseline and not args.no_fill:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = _cpu_baseline("l80" if w.shape.num_layers == 80 else "l32")

@@ -7,6 +7,7 @@ formula, never from the GPU.
 """
 from __future__ import annotations
 
+import time
 from typing import Dict, List, Optional
 
 import numpy as np
@@ -48,15 +49,30 @@ class OraclePath:
             self.index[int(h[boff[p] + (j + 1) * self.bpc - 1])] = slot
         self.free = list(range(len(w.prestage_chunks), w.num_slots))
 
-    def run_pass(self, evict_stored: bool = False) -> dict:
+    def run_pass(self, evict_stored: bool = False, timers: Optional[dict] = None) -> dict:
+        """One pass.  ``timers``: optional dict; wall seconds of each step are
+        added under "hash", "lookup" (lookup and job build), "retrieve" and
+        "store"."""
         w = self.batch
+        clock = [time.perf_counter()]
+
+        def lap(name):
+            if timers is not None:
+                now = time.perf_counter()
+                timers[name] = timers.get(name, 0.0) + now - clock[0]
+                clock[0] = now
+
         bh = oracle.hash_prefix(w.tokens, w.tok_off, self.hash_seed, self.blk_off)
+        lap("hash")
         cs, hit = oracle.lookup(self.index, bh, self.blk_off, self.bpc, self.chunk_off)
         retr, store, skeys, dropped = oracle.build_jobs(hit, cs, bh, self.blk_off, self.chunk_off, self.bpc,
                                                         np.array(self.free, np.int32))
+        lap("lookup")
         if self.staging is not None:
             oracle.retrieve_scatter(self.layout, self.staging, self.layers, w.block_tables, retr)
+            lap("retrieve")
             oracle.store_gather(self.layout, self.staging, self.layers, w.block_tables, store)
+            lap("store")
         for k, s in zip(skeys, store[:, 0]):
             self.index[int(k)] = int(s)
         used = set(int(s) for s in store[:, 0])
