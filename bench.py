@@ -7,6 +7,9 @@ decisions, one host-to-device copy of the jobs, the retrieve scatter, the
 store gather, and the index update (the chunks stored in the step are evicted
 again at its end, so every step does the same work).  Inputs (tokens, block
 tables, staging and pool contents) are resident in HBM before timing starts.
+Steps overlap as in a serving loop: the hash and lookup of step i+1 run on a
+stream of their own, and its jobs are built on the host, while the copies of
+step i are in flight (--serial runs them back to back).
 
 Prints one JSON line: the whole-step payload rate in GB/s (bytes read plus
 bytes written by the scatter and the gather, divided by wall time per step),
@@ -294,6 +297,9 @@ def main() -> int:
                          "with no chunk resident in HBM")
     ap.add_argument("--slots-per-batch", type=int, default=4,
                     help="staged modes: distinct staged chunks per copy/scatter batch")
+    ap.add_argument("--serial", action="store_true",
+                    help="run each step's hash and lookup after the previous step's copies instead of overlapping "
+                         "them (with the host job build) with those copies")
     ap.add_argument("--no-fill", action="store_true",
                     help="leave KV buffers uninitialised (hardware-counter runs: no generator kernels run; the "
                          "copies move the same bytes) and skip the device-copy and CPU-baseline extras")
@@ -325,25 +331,50 @@ def main() -> int:
     w = W.make(args.workload)
     print(f"[bench] workload {w.name}: {w.num_reqs} requests, pool {w.pool_bytes() / 2**30:.1f} GiB, "
           f"staging {w.staged_bytes() / 2**30:.1f} GiB", file=sys.stderr, flush=True)
-    path = StagingPath(w, lower_tier=args.lower_tier, slots_per_batch=args.slots_per_batch)
+    path = StagingPath(w, lower_tier=args.lower_tier, slots_per_batch=args.slots_per_batch,
+                       overlap=not args.serial)
     if not args.no_fill:
         path.fill(STG_TAG, POOL_TAG, w.seed)
     path.prestage()
-    for _ in range(args.warmup):
-        path.drop_fast_tier()
-        path.run_pass(evict_stored=True)
+
+    def steps(n, timers=None):
+        # Step i+1's hash and lookup are enqueued (on their own stream) as soon
+        # as step i's copies and index update are, so they and step i+1's host
+        # job build overlap step i's copies.  Every step still does all its work.
+        out = None
+        if n:
+            path.launch_lookup(timers)
+        for i in range(n):
+            path.drop_fast_tier()          # staged modes: every step stages its chunks again
+            out = path.complete_pass(evict_stored=True, timers=timers)
+            if i + 1 < n:
+                path.launch_lookup(timers)
+        return out
+
+    steps(args.warmup)
+    torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
 
     timers: dict = {}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    stats = None
-    for _ in range(args.steps):
-        path.drop_fast_tier()          # staged modes: every step stages its chunks again
-        stats = path.run_pass(evict_stored=True, timers=timers)
+    stats = steps(args.steps, timers)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     print(f"[bench] timed {args.steps} steps", file=sys.stderr, flush=True)
+
+    # hash and lookup once more on an otherwise idle GPU: in the overlapped
+    # steps they share the CUs with the previous step's copies
+    iso: dict = {}
+    path.set_overlap(False)
+    for _ in range(5):
+        path.drop_fast_tier()
+        path.run_pass(evict_stored=True, timers=iso)
+    torch.cuda.synchronize()
+
+    def iso_ms(name):
+        ev = [a.elapsed_time(b) for a, b in iso.get(name, [])]
+        return float(np.median(ev)) if ev else 0.0
 
     def avg_ms(name):
         ev = timers.get(name, [])
@@ -361,7 +392,8 @@ def main() -> int:
     r_gbs = r_bytes / (k_ms["retrieve"] * 1e-3) / 1e9 if k_ms["retrieve"] else 0.0
     s_gbs = s_bytes / (k_ms["store"] * 1e-3) / 1e9 if k_ms["store"] else 0.0
     n_tok = int(w.tokens.size)
-    hash_mtok = n_tok / (k_ms["hash"] * 1e-3) / 1e6 if k_ms["hash"] else 0.0
+    hash_iso = iso_ms("hash")
+    hash_mtok = n_tok / (hash_iso * 1e-3) / 1e6 if hash_iso else 0.0
 
     dom = "retrieve" if k_ms["retrieve"] * 1 >= k_ms["store"] else "store"
     dom_kernel = "kv_copy_retrieve" if dom == "retrieve" else "kv_copy_store"
@@ -386,7 +418,8 @@ def main() -> int:
                    "head_dim": w.shape.head_dim, "block_size": w.shape.block_size,
                    "chunk_tokens": w.shape.chunk_tokens, "requests": w.num_reqs, "tokens": n_tok,
                    "pool_blocks": w.num_blocks, "staging_slots": w.num_slots,
-                   "retrieve_jobs": stats.num_retrieve, "store_jobs": stats.num_store},
+                   "retrieve_jobs": stats.num_retrieve, "store_jobs": stats.num_store,
+                   "steps_overlap": not args.serial},
         "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic},
         "kernels": {
@@ -395,11 +428,14 @@ def main() -> int:
                                  "payload_bytes_rw": r_bytes, "unique_min_bytes": uniq + stats.retrieve_bytes},
             "store_gather": {"ms": round(k_ms["store"], 4), "GB/s": round(s_gbs, 1),
                              "frac_of_peak": round(s_gbs / HBM_PEAK_GBS, 4), "payload_bytes_rw": s_bytes},
-            "hash_prefix": {"ms": round(k_ms["hash"], 4), "Mtok/s": round(hash_mtok, 1),
-                            "ns_per_chain_step": round(k_ms["hash"] * 1e6 / max(1, int(w.lengths.max()) // 16), 2)},
-            "lookup": {"ms": round(k_ms["lookup"], 4)},
+            "hash_prefix": {"ms": round(k_ms["hash"], 4), "isolated_ms": round(hash_iso, 4),
+                            "Mtok/s": round(hash_mtok, 1),
+                            "ns_per_chain_step": round(hash_iso * 1e6 / max(1, int(w.lengths.max()) // 16), 2)},
+            "lookup": {"ms": round(k_ms["lookup"], 4), "isolated_ms": round(iso_ms("lookup"), 4)},
         },
-        "timing": "HIP events on the launch stream around every launch of the timed steps; ms = mean",
+        "timing": "HIP events on the launch stream around every launch of the timed steps (ms = mean); hash "
+                  "and lookup also on an idle GPU after the timed steps (isolated_ms = median of 5, used for "
+                  "Mtok/s)",
         "source_digest": _src_digest(),
     }
     for name, key in (("retrieve", "retrieve_scatter"), ("store", "store_gather"), ("hash", "hash_prefix"),

@@ -303,6 +303,19 @@ int kv_commit_should_stage(double ttu_s, double ttr_s, uint64_t free_protected_b
                            uint64_t claim_new_bytes, uint64_t claim_total_bytes,
                            uint64_t budget_bytes, int retrieval_requested);
 
+/* The same rule for the n claims of one batch, each decided on its own
+ * against the same free protected capacity and budget:
+ *   h_out[i] = kv_commit_should_stage(h_ttu[i], h_ttr[i], free_protected_bytes,
+ *                                     h_claim_new[i], h_claim_total[i],
+ *                                     budget_bytes, h_requested[i])
+ * (h_requested: one byte per claim, nonzero = retrieval requested).  An
+ * element with invalid inputs gets KV_EINVAL in h_out; the others are still
+ * decided.  Host arrays only; nothing is kept.  Returns KV_OK, or KV_EINVAL
+ * for n < 0 or a null array with n > 0. */
+int kv_commit_should_stage_n(int32_t n, const double *h_ttu, const double *h_ttr, uint64_t free_protected_bytes,
+                             const uint64_t *h_claim_new, const uint64_t *h_claim_total, uint64_t budget_bytes,
+                             const uint8_t *h_requested, int32_t *h_out);
+
 /* ----------------------------------------------------------------------- */
 /* Claim controller and staging simulator (host)                            */
 /* ----------------------------------------------------------------------- */

@@ -30,7 +30,7 @@ HASH_BLOCK_TOKENS = 16
 EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
            "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
            "kv_store_gather", "kv_group_jobs_by_slot", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
-           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out", "kv_pipeline_create",
+           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out", "kv_pipeline_create", "kv_commit_should_stage_n",
            "kv_pipeline_destroy", "kv_retrieve_pipelined"]
 
 
@@ -96,6 +96,7 @@ def lib() -> ct.CDLL:
         "kv_group_jobs_by_slot": [_vp, _i32],
         "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
         "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
+        "kv_commit_should_stage_n": [_i32, _vp, _vp, _u64, _vp, _vp, _u64, _vp, _vp],
         "kv_strerror": [ct.c_int],
         "kv_host_device_pointer": [_vp, ct.POINTER(_vp)],
         "kv_version": [],
@@ -421,6 +422,26 @@ def kv_commit_should_stage(ttu_s: float, ttr_s: float, free_protected_bytes: int
     """Returns a KV_DEFER/KV_COMMIT/KV_BLOCKED/KV_ORDINARY decision or KV_EINVAL."""
     return lib().kv_commit_should_stage(ttu_s, ttr_s, free_protected_bytes, claim_new_bytes, claim_total_bytes,
                                         budget_bytes, 1 if retrieval_requested else 0)
+
+
+def kv_commit_should_stage_n(ttu, ttr, free_protected_bytes: int, claim_new, claim_total, budget_bytes: int,
+                             requested) -> np.ndarray:
+    """The commitment rule for a batch of claims (int32 decisions, KV_EINVAL
+    for an element with invalid inputs)."""
+    a = np.ascontiguousarray(ttu, np.float64).reshape(-1)
+    n = a.size
+    b = np.ascontiguousarray(ttr, np.float64).reshape(-1)
+    cn = np.ascontiguousarray(claim_new, np.uint64).reshape(-1)
+    ct_ = np.ascontiguousarray(claim_total, np.uint64).reshape(-1)
+    rq = np.ascontiguousarray(np.asarray(requested).astype(bool), np.uint8).reshape(-1)
+    if not (b.size == cn.size == ct_.size == rq.size == n):
+        raise ValueError("all claim arrays must have the same length")
+    out = np.zeros(n, np.int32)
+    if n:
+        _check(lib().kv_commit_should_stage_n(n, a.ctypes.data, b.ctypes.data, int(free_protected_bytes),
+                                              cn.ctypes.data, ct_.ctypes.data, int(budget_bytes), rq.ctypes.data,
+                                              out.ctypes.data), "kv_commit_should_stage_n")
+    return out
 
 
 def kv_host_device_pointer(host_ptr: int) -> int:

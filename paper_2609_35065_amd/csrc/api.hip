@@ -217,6 +217,17 @@ int kv_commit_should_stage(double ttu_s, double ttr_s, uint64_t free_protected_b
     return retrieval_requested ? KV_ORDINARY : KV_BLOCKED;
 }
 
+int kv_commit_should_stage_n(int32_t n, const double *h_ttu, const double *h_ttr, uint64_t free_protected_bytes,
+                             const uint64_t *h_claim_new, const uint64_t *h_claim_total, uint64_t budget_bytes,
+                             const uint8_t *h_requested, int32_t *h_out) {
+    if (n < 0) return KV_EINVAL;
+    if (n > 0 && (!h_ttu || !h_ttr || !h_claim_new || !h_claim_total || !h_requested || !h_out)) return KV_EINVAL;
+    for (int32_t i = 0; i < n; ++i)
+        h_out[i] = kv_commit_should_stage(h_ttu[i], h_ttr[i], free_protected_bytes, h_claim_new[i], h_claim_total[i],
+                                          budget_bytes, h_requested[i] != 0);
+    return KV_OK;
+}
+
 const char *kv_strerror(int status) {
     switch (status) {
     case KV_OK: return "ok";

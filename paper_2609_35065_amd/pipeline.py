@@ -2,7 +2,7 @@
 
 A pass is:  hash (kv_hash_prefix) -> lookup (kv_lookup) -> one device-to-host
 copy of the lookup result -> host job build (kv_build_jobs) and commitment
-decisions (kv_commit_should_stage) -> one host-to-device copy of the jobs ->
+decisions (kv_commit_should_stage_n) -> one host-to-device copy of the jobs ->
 retrieve scatter (kv_retrieve_scatter) -> store gather (kv_store_gather) ->
 index update (kv_index_insert; optionally kv_index_erase of what was just
 stored, which returns the batch to its starting state so that passes can be
@@ -31,7 +31,7 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, KvPipeline, kv_build_jobs, kv_commit_should_stage,
+from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, KvPipeline, kv_build_jobs, kv_commit_should_stage_n,
                kv_group_jobs_by_slot, kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_pipelined,
                kv_retrieve_scatter, kv_stage_out, kv_store_gather, make_layout)
 
@@ -60,13 +60,18 @@ class StagingPath:
     the start.  KV contents are filled by the caller (see ``fill``)."""
 
     def __init__(self, w, device: str = "cuda", hash_seed: int = 0, stream: Optional[torch.cuda.Stream] = None,
-                 lower_tier: str = "zero-copy", slots_per_batch: int = 4):
+                 lower_tier: str = "zero-copy", slots_per_batch: int = 4, overlap: bool = False):
         if lower_tier not in LOWER_TIER_MODES:
             raise ValueError(f"lower_tier must be one of {LOWER_TIER_MODES}")
         self.w = w
         self.dev = torch.device(device)
         self.hash_seed = hash_seed
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.dev)
+        # hash, lookup and index updates; a stream of their own when passes overlap
+        self._own_lookup_stream = torch.cuda.Stream(self.dev)
+        self.lookup_stream = self._own_lookup_stream if overlap else self.stream
+        self._lookup_done = torch.cuda.Event()
+        self._parity = 0
         s = w.shape
         kv_stride, block_stride = w.strides()
         self.layout: KvLayout = make_layout(s.num_layers, s.kv_heads, s.head_dim, s.elem_bytes, s.block_size,
@@ -125,15 +130,26 @@ class StagingPath:
         self.h_block_hash = torch.zeros(max(nblk, 1), dtype=torch.int64, pin_memory=True)
         self.h_chunk_slot = torch.zeros(max(nch, 1), dtype=torch.int32, pin_memory=True)
         self.h_hit = torch.zeros(max(R, 1), dtype=torch.int32, pin_memory=True)
-        self.h_retr = torch.zeros((max(nch, 1), 4), dtype=torch.int32, pin_memory=True)
-        self.h_store = torch.zeros((max(nch, 1), 4), dtype=torch.int32, pin_memory=True)
+        # job lists, two of each: a pass fills one while the upload of the other may still be queued
+        self._h_retr = [torch.zeros((max(nch, 1), 4), dtype=torch.int32, pin_memory=True) for _ in range(2)]
+        self._h_store = [torch.zeros((max(nch, 1), 4), dtype=torch.int32, pin_memory=True) for _ in range(2)]
+        self._uploaded = [torch.cuda.Event(), torch.cuda.Event()]
         self.stream.synchronize()
+        self.lookup_stream.synchronize()
 
     # ------------------------------------------------------------------
     def staging_view(self) -> torch.Tensor:
         """The authoritative staged chunks: the host buffer when the workload
         keeps them in host memory, else the HBM staging buffer."""
         return self.staging_host if self.staging_host is not None else self.staging
+
+    def set_overlap(self, overlap: bool) -> None:
+        """Run hash, lookup and index updates on a stream of their own (passes
+        can overlap) or on this path's stream (each pass after the previous
+        one's copies).  Waits for all queued work first."""
+        self.stream.synchronize()
+        self.lookup_stream.synchronize()
+        self.lookup_stream = self._own_lookup_stream if overlap else self.stream
 
     def drop_fast_tier(self) -> None:
         """Forget which slots are resident in HBM (staged modes): the next
@@ -181,9 +197,10 @@ class StagingPath:
                 kv_hash_prefix(dt, doff, off.size - 1, self.hash_seed, dboff, dh, self.stream)
                 h = dh.cpu().numpy().view(np.uint64)
             keys = np.array([h[boff[p] + (j + 1) * self.bpc - 1] for p, j in w.prestage_chunks], np.uint64)
-            self.index.insert(keys, np.arange(P, dtype=np.int32), self.stream)
+            self.index.insert(keys, np.arange(P, dtype=np.int32), self.lookup_stream)
         self.free = list(range(P, w.num_slots))
         self.stream.synchronize()
+        self.lookup_stream.synchronize()
 
     # ------------------------------------------------------------------
     def run_pass(self, evict_stored: bool = False, validate: bool = False, timers: Optional[dict] = None) -> PassStats:
@@ -191,23 +208,41 @@ class StagingPath:
 
         ``timers``: optional dict; when given, a (start, end) pair of
         torch.cuda.Event is appended under "hash", "lookup", "retrieve" and
-        "store" around each launch, recorded on this path's stream."""
+        "store" around each launch, recorded on the stream it runs on."""
+        self.launch_lookup(timers)
+        return self.complete_pass(evict_stored, validate, timers)
+
+    def launch_lookup(self, timers: Optional[dict] = None) -> None:
+        """Enqueue the first half of a pass on the lookup stream: hash, lookup
+        and the copy of their results to pinned host memory.  It sees every
+        index update enqueued before it.  With overlapping passes it runs
+        while the copies of the previous pass are still in flight."""
+        w = self.batch
+        R = w.num_reqs
+        ls = self.lookup_stream
+        with torch.cuda.stream(ls):
+            e = self._ev(timers, "hash", ls)
+            kv_hash_prefix(self.tokens, self.tok_off, R, self.hash_seed, self.blk_off, self.block_hash, ls)
+            self._ev_end(e, ls)
+            e = self._ev(timers, "lookup", ls)
+            kv_lookup(self.index, self.block_hash, self.blk_off, R, self.bpc, self.chunk_off, self.chunk_slot,
+                      self.hit, ls)
+            self._ev_end(e, ls)
+            self.h_block_hash.copy_(self.block_hash, non_blocking=True)
+            self.h_chunk_slot.copy_(self.chunk_slot, non_blocking=True)
+            self.h_hit.copy_(self.hit, non_blocking=True)
+            self._lookup_done.record(ls)
+
+    def complete_pass(self, evict_stored: bool = False, validate: bool = False,
+                      timers: Optional[dict] = None) -> PassStats:
+        """Second half of a pass: wait for the lookup results, build the jobs
+        and decisions on the host, enqueue the copies on this path's stream
+        and the index update on the lookup stream."""
         w = self.batch
         R = w.num_reqs
         st = PassStats()
         nblk, nch = int(self.blk_off_h[-1]), int(self.chunk_off_h[-1])
-        with torch.cuda.stream(self.stream):
-            e = self._ev(timers, "hash")
-            kv_hash_prefix(self.tokens, self.tok_off, R, self.hash_seed, self.blk_off, self.block_hash, self.stream)
-            self._ev_end(e)
-            e = self._ev(timers, "lookup")
-            kv_lookup(self.index, self.block_hash, self.blk_off, R, self.bpc, self.chunk_off, self.chunk_slot,
-                      self.hit, self.stream)
-            self._ev_end(e)
-            self.h_block_hash.copy_(self.block_hash, non_blocking=True)
-            self.h_chunk_slot.copy_(self.chunk_slot, non_blocking=True)
-            self.h_hit.copy_(self.hit, non_blocking=True)
-        self.stream.synchronize()
+        self._lookup_done.synchronize()
         bh = self.h_block_hash.numpy()[:nblk].view(np.uint64)
         cs = self.h_chunk_slot.numpy()[:nch]
         hit = self.h_hit.numpy()[:R]
@@ -220,17 +255,25 @@ class StagingPath:
         # commitment decision per request claim: retrieval is requested now;
         # the claim's matched footprint must fit the staged capacity
         budget = self.w.num_slots * slot_bytes
-        for r in range(R):
-            if hit[r] > 0:
-                d = kv_commit_should_stage(0.0, 0.0, budget, 0, int(hit[r]) * slot_bytes, budget, True)
-                st.decisions[d] = st.decisions.get(d, 0) + 1
-                st.commits += int(d == KV_COMMIT)
+        claims = np.nonzero(hit > 0)[0]
+        if claims.size:
+            total = hit[claims].astype(np.uint64) * np.uint64(slot_bytes)
+            dec = kv_commit_should_stage_n(np.zeros(claims.size), np.zeros(claims.size), budget,
+                                           np.zeros(claims.size, np.uint64), total, budget,
+                                           np.ones(claims.size, bool))
+            for d, c in zip(*np.unique(dec, return_counts=True)):
+                st.decisions[int(d)] = int(c)
+            st.commits = int(np.count_nonzero(dec == KV_COMMIT))
         if validate:
             from . import kv_validate_jobs
             assert kv_validate_jobs(self.layout, w.block_tables, retr, False) == 0 or len(retr) == 0
             assert kv_validate_jobs(self.layout, w.block_tables, store, True) == 0 or len(store) == 0
         nr, ns = len(retr), len(store)
         nres = nr   # jobs whose chunk is already in the staging buffer the scatter reads
+        par = self._parity
+        self._parity ^= 1
+        self._uploaded[par].synchronize()     # the upload that last read these buffers has run
+        self.h_retr, self.h_store = self._h_retr[par], self._h_store[par]
         with torch.cuda.stream(self.stream):
             if nr:
                 # jobs sharing a staged chunk run back to back (results do not depend on order)
@@ -245,6 +288,7 @@ class StagingPath:
             if ns:
                 self.h_store.numpy()[:ns] = store
                 self.d_store[:ns].copy_(self.h_store[:ns], non_blocking=True)
+            self._uploaded[par].record(self.stream)
             e = self._ev(timers, "retrieve")
             kv_retrieve_scatter(self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_retr,
                                 nres, self.stream)
@@ -270,8 +314,8 @@ class StagingPath:
                 kv_stage_out(self.layout, self.staging, self.staging_host, np.sort(store[:, 0]), self.stream)
                 self.resident[store[:, 0]] = True
             self._ev_end(e)
-            if ns:
-                self.index.insert(skeys, store[:, 0].copy(), self.stream)
+        if ns:
+            self.index.insert(skeys, store[:, 0].copy(), self.lookup_stream)
         used = set(int(x) for x in store[:, 0])
         self.free = [s for s in self.free if s not in used]
         self.last_store_keys, self.last_store_slots = skeys, store[:, 0].copy()
@@ -295,8 +339,7 @@ class StagingPath:
     def evict_last(self) -> None:
         """Erase the keys stored by the last pass and free their slots."""
         if self.last_store_keys.size:
-            with torch.cuda.stream(self.stream):
-                self.index.erase(self.last_store_keys, self.stream)
+            self.index.erase(self.last_store_keys, self.lookup_stream)
             self.free = sorted(self.free + [int(s) for s in self.last_store_slots])
             self.last_store_keys = np.zeros(0, np.uint64)
             self.last_store_slots = np.zeros(0, np.int32)

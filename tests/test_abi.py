@@ -50,6 +50,28 @@ def test_commit_rule_matches_oracle(seed):
             oracle.commit_should_stage(ttu, ttr, free, new, total, budget, req)
 
 
+@pytest.mark.parametrize("seed", range(6))
+def test_batched_commit_rule_matches_oracle_elementwise(seed):
+    rng = np.random.default_rng(50 + seed)
+    vals = np.array([-math.inf, -1.0, 0.0, 0.5, 1.0, 2.0, math.inf, math.nan])
+    n = 400
+    ttu, ttr = rng.choice(vals, n), rng.choice(vals, n)
+    new = rng.integers(0, 12, n).astype(np.uint64)
+    total = rng.integers(0, 12, n).astype(np.uint64)
+    req = rng.integers(0, 2, n).astype(bool)
+    free, budget = (int(x) for x in rng.integers(0, 12, 2))
+    got = kv.kv_commit_should_stage_n(ttu, ttr, free, new, total, budget, req)
+    exp = [oracle.commit_should_stage(float(ttu[i]), float(ttr[i]), free, int(new[i]), int(total[i]), budget,
+                                      bool(req[i])) for i in range(n)]
+    assert got.tolist() == exp
+    assert kv.KV_EINVAL in exp and kv.KV_COMMIT in exp           # invalid elements do not stop the batch
+    assert kv.kv_commit_should_stage_n([], [], 0, [], [], 0, []).size == 0
+    L = kv.lib()
+    assert L.kv_commit_should_stage_n(-1, None, None, 0, None, None, 0, None, None) == kv.KV_EINVAL
+    assert L.kv_commit_should_stage_n(3, None, None, 0, None, None, 0, None, None) == kv.KV_EINVAL
+    assert L.kv_commit_should_stage_n(0, None, None, 0, None, None, 0, None, None) == kv.KV_OK
+
+
 def _lookup_case(seed):
     rng = np.random.default_rng(seed)
     C = int(rng.choice([16, 32, 64]))

@@ -317,3 +317,33 @@ def test_host_staging_zero_copy(layout):
     for p in range(2):
         sg, so = g.run_pass(validate=True), o.run_pass()
         _compare_pass(g, o, sg, so)
+
+
+@pytest.mark.parametrize("evict", [False, True])
+def test_overlapped_passes_match_sequential_oracle(evict):
+    # Hash and lookup of pass i+1 are enqueued on their own stream right after
+    # pass i's copies and index update; the jobs and every byte must be those
+    # of the oracle's passes run one after another.
+    shape = W.KVShape(2, 2, 64, 2, 16, 64)
+    w = W.small_random(77, shape, num_reqs=9, max_len=5 * 64 + 21)
+    g = StagingPath(w, overlap=True)
+    g.fill(STG_TAG, POOL_TAG, w.seed, True)
+    g.prestage()
+    o = OraclePath(w, kv_seed=w.seed, finite=True, staging_tag=STG_TAG, pool_tag_base=POOL_TAG)
+    o.prestage()
+    assert g.lookup_stream is not g.stream
+    n = 4
+    g.launch_lookup()
+    for i in range(n):
+        sg = g.complete_pass(evict_stored=evict, validate=True)
+        so = o.run_pass(evict_stored=evict)
+        assert np.array_equal(g.last_retrieve, so["retrieve"]), i
+        assert np.array_equal(g.last_store, so["store"]), i
+        assert sg.dropped == so["dropped"]
+        if i + 1 < n:
+            g.launch_lookup()
+    torch.cuda.synchronize()
+    assert np.array_equal(g.staging_view().cpu().numpy(), o.staging)
+    for l in range(len(g.layers)):
+        assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
+    _free(g, o)
