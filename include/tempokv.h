@@ -22,8 +22,10 @@
  * --------------------------------
  *  - Pointers named d_* are device-accessible (HBM, or mapped pinned host
  *    memory for the staging buffer); h_* are host memory.  The caller owns
- *    every buffer.  No call on the hot path allocates memory or keeps a
- *    pointer after it returns.
+ *    every buffer.  No call on the hot path allocates device or pinned host
+ *    memory (kv_index_create allocates the index's device table and pinned
+ *    snapshots, kv_pipeline_create its events; host-side calls use ordinary
+ *    heap temporaries) or keeps a pointer after it returns.
  *  - GPU calls enqueue work on `stream` (a hipStream_t; NULL = the default
  *    stream) and return without synchronising.  Device faults surface at the
  *    caller's next synchronisation.

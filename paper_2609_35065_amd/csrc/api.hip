@@ -16,8 +16,10 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 }  // namespace
 
+namespace tkv {
+
 // Layout checks shared by the copy directions and staging.
-int tkv::check_layout(const kv_layout *lo) {
+int check_layout(const kv_layout *lo) {
     if (!lo) return KV_EINVAL;
     if (lo->num_layers <= 0 || lo->num_layers > KV_MAX_LAYERS || lo->kv_heads <= 0 || lo->head_dim <= 0 ||
         lo->block_size <= 0 || lo->chunk_tokens <= 0 || lo->num_blocks <= 0 || lo->num_slots <= 0)
@@ -35,13 +37,8 @@ int tkv::check_layout(const kv_layout *lo) {
     return KV_OK;
 }
 
-namespace {
-using tkv::check_layout;
-
-}  // namespace
-
-namespace tkv {
-int make_copy_params(tkv::CopyParams &p, const kv_layout *lo, const void *staging, const void *const *layers,
+// Launch parameters of one copy call, after every argument check.
+int make_copy_params(CopyParams &p, const kv_layout *lo, const void *staging, const void *const *layers,
                      const int32_t *bt, int32_t bt_stride, int32_t num_reqs, const kv_job *jobs,
                      int32_t num_jobs) {
     int rc = check_layout(lo);
@@ -73,11 +70,11 @@ int make_copy_params(tkv::CopyParams &p, const kv_layout *lo, const void *stagin
     p.total_segs = (int64_t)num_jobs * lo->num_layers * 2 * nseg;
     return KV_OK;
 }
+
 }  // namespace tkv
 
-namespace {
+using tkv::check_layout;
 using tkv::make_copy_params;
-}  // namespace
 
 extern "C" {
 
