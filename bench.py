@@ -395,12 +395,16 @@ def main() -> int:
     hash_iso = iso_ms("hash")
     hash_mtok = n_tok / (hash_iso * 1e-3) / 1e6 if hash_iso else 0.0
 
+    # unique staged bytes a retrieve must read at least once + bytes written:
+    # its algorithmic HBM bytes when requests share staged chunks (the
+    # counters measure within 0.2 % of this); the payload counts every read
+    uniq = len(set(int(q[0]) for q in path.last_retrieve)) * w.shape.slot_bytes
+    r_alg = uniq + stats.retrieve_bytes
+    r_hbm = r_alg / (k_ms["retrieve"] * 1e-3) / 1e9 if k_ms["retrieve"] else 0.0
     dom = "retrieve" if k_ms["retrieve"] * 1 >= k_ms["store"] else "store"
     dom_kernel = "kv_copy_retrieve" if dom == "retrieve" else "kv_copy_store"
-    achieved = r_gbs if dom == "retrieve" else s_gbs
+    achieved = r_hbm if dom == "retrieve" else s_gbs
     traffic = _load_traffic(dom_kernel, args.workload)
-    # unique staged bytes a retrieve must read at least once + bytes written
-    uniq = len(set(int(q[0]) for q in path.last_retrieve)) * w.shape.slot_bytes
     line = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -423,9 +427,9 @@ def main() -> int:
         "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic},
         "kernels": {
-            "retrieve_scatter": {"ms": round(k_ms["retrieve"], 4), "GB/s": round(r_gbs, 1),
-                                 "frac_of_peak": round(r_gbs / HBM_PEAK_GBS, 4),
-                                 "payload_bytes_rw": r_bytes, "unique_min_bytes": uniq + stats.retrieve_bytes},
+            "retrieve_scatter": {"ms": round(k_ms["retrieve"], 4), "GB/s": round(r_hbm, 1),
+                                 "frac_of_peak": round(r_hbm / HBM_PEAK_GBS, 4), "algorithmic_bytes": r_alg,
+                                 "payload_GB/s": round(r_gbs, 1), "payload_bytes_rw": r_bytes},
             "store_gather": {"ms": round(k_ms["store"], 4), "GB/s": round(s_gbs, 1),
                              "frac_of_peak": round(s_gbs / HBM_PEAK_GBS, 4), "payload_bytes_rw": s_bytes},
             "hash_prefix": {"ms": round(k_ms["hash"], 4), "isolated_ms": round(hash_iso, 4),
