@@ -120,9 +120,16 @@ def test_tiny_store_one_request_then_partial_hits():
 # random small workloads over shapes and layouts
 # ---------------------------------------------------------------------------
 
+# Segment sizes B*H*D*e cover every copy path: 4 KiB rows x 1, 2, 4, 8, 16 (retrieve) and 16/8/4 KiB rows
+# (store), and sizes that are none of these (generic path); also fp8 and fp32 elements, a head size that is
+# not a power of two, and the largest layer count a layout may name.
 SHAPES = [W.KVShape(2, 2, 64, 2, 16, 64), W.KVShape(3, 1, 64, 2, 16, 16), W.KVShape(1, 8, 128, 2, 16, 256),
           W.KVShape(2, 2, 128, 2, 32, 128), W.KVShape(2, 1, 64, 1, 32, 32), W.KVShape(1, 2, 64, 4, 16, 64),
-          W.KVShape(4, 8, 64, 2, 32, 512), W.KVShape(2, 1, 128, 2, 16, 16)]
+          W.KVShape(4, 8, 64, 2, 32, 512), W.KVShape(2, 1, 128, 2, 16, 16),
+          W.KVShape(2, 8, 128, 2, 32, 64),        # 64 KiB segments
+          W.KVShape(1, 3, 80, 4, 16, 32),         # 15 KiB segments, fp32, head size 80
+          W.KVShape(2, 4, 128, 1, 16, 64),        # fp8 elements, 8 KiB segments
+          W.KVShape(128, 1, 16, 2, 16, 16)]       # 128 layers of 512-byte segments
 
 
 @pytest.mark.parametrize("layout,pad", [("kv_first", 0), ("block_first", 0), ("kv_first", 4096), ("block_first", 48)])
