@@ -6,18 +6,30 @@
 // (linear probing from a Fibonacci-hashed home position, tombstones for
 // erased keys), so a mutation is mirrored by uploading the table image.
 //
-// Uploads are stream-ordered: the table image is copied into one of two
-// pinned snapshot buffers and sent with hipMemcpyAsync on the caller's
-// stream, so a lookup enqueued after an insert on the same stream sees the
-// insert.  A snapshot buffer is reused only after the event recorded behind
-// its previous upload has completed.
+// Uploads are stream-ordered, so a lookup enqueued after an insert on the
+// same stream sees the insert.  A mutation that changed few entries uploads
+// only those: (position, entry) pairs go through a pinned snapshot buffer to
+// a device list, and a small kernel writes them into the table.  After a
+// rehash, or when many entries changed, the whole table image is sent
+// instead.  Each of the two snapshot buffers (and its device list) is reused
+// only after the event recorded behind its previous upload has completed.
 
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
 #include "internal.h"
+
+namespace tkv {
+// One changed table entry, as uploaded by an incremental update.
+struct alignas(16) IndexUpdate {
+    int64_t pos;
+    int64_t pad;
+    IndexEntry entry;
+};
+}  // namespace tkv
 
 struct kv_index {
     int device = 0;
@@ -29,6 +41,10 @@ struct kv_index {
     std::vector<tkv::IndexEntry> host;
     tkv::IndexEntry *dev = nullptr;
     tkv::IndexEntry *snap[2] = {nullptr, nullptr};
+    tkv::IndexUpdate *dev_upd[2] = {nullptr, nullptr};
+    int64_t upd_cap = 0;             // pairs per incremental upload
+    std::vector<int64_t> dirty;      // positions changed since the last upload
+    bool full = true;                // the next upload sends the whole table
     hipEvent_t ev[2] = {nullptr, nullptr};
     bool ev_used[2] = {false, false};
     int next = 0;
@@ -37,6 +53,7 @@ struct kv_index {
 namespace {
 
 using tkv::IndexEntry;
+using tkv::IndexUpdate;
 using tkv::kEmpty;
 using tkv::kLive;
 using tkv::kTomb;
@@ -65,7 +82,19 @@ int64_t probe(const kv_index *ix, uint64_t key, int64_t *free_pos) {
     return -1;
 }
 
+constexpr int kApplyThreads = 256;
+
+__global__ __launch_bounds__(kApplyThreads) void index_apply_kernel(const IndexUpdate *__restrict__ upd, int64_t n,
+                                                                   int64_t cap, IndexEntry *__restrict__ table) {
+    const int64_t i = (int64_t)blockIdx.x * kApplyThreads + threadIdx.x;
+    if (i >= n) return;
+    const int64_t pos = upd[i].pos;
+    if (pos >= 0 && pos < cap) table[pos] = upd[i].entry;
+}
+
 void rehash(kv_index *ix) {
+    ix->full = true;
+    ix->dirty.clear();
     std::vector<IndexEntry> old;
     old.swap(ix->host);
     ix->host.assign(ix->cap, IndexEntry{0, -1, kEmpty});
@@ -87,13 +116,35 @@ int upload(kv_index *ix, hipStream_t stream) {
     const int k = ix->next;
     const size_t bytes = sizeof(IndexEntry) * (size_t)ix->cap;
     if (ix->ev_used[k] && hipEventSynchronize(ix->ev[k]) != hipSuccess) rc = KV_EHIP;
-    if (rc == KV_OK) {
+    std::sort(ix->dirty.begin(), ix->dirty.end());
+    ix->dirty.erase(std::unique(ix->dirty.begin(), ix->dirty.end()), ix->dirty.end());
+    const int64_t n = (int64_t)ix->dirty.size();
+    if (rc == KV_OK && (ix->full || n > ix->upd_cap)) {
         memcpy(ix->snap[k], ix->host.data(), bytes);
         if (hipMemcpyAsync(ix->dev, ix->snap[k], bytes, hipMemcpyHostToDevice, stream) != hipSuccess ||
             hipEventRecord(ix->ev[k], stream) != hipSuccess)
             rc = KV_EHIP;
         else
             ix->ev_used[k] = true;
+    } else if (rc == KV_OK && n > 0) {
+        IndexUpdate *list = reinterpret_cast<IndexUpdate *>(ix->snap[k]);
+        for (int64_t i = 0; i < n; ++i) list[i] = IndexUpdate{ix->dirty[i], 0, ix->host[ix->dirty[i]]};
+        (void)hipGetLastError();
+        if (hipMemcpyAsync(ix->dev_upd[k], list, sizeof(IndexUpdate) * (size_t)n, hipMemcpyHostToDevice, stream) !=
+            hipSuccess) {
+            rc = KV_EHIP;
+        } else {
+            hipLaunchKernelGGL(index_apply_kernel, dim3((unsigned)((n + kApplyThreads - 1) / kApplyThreads)),
+                               dim3(kApplyThreads), 0, stream, ix->dev_upd[k], n, ix->cap, ix->dev);
+            if (hipGetLastError() != hipSuccess || hipEventRecord(ix->ev[k], stream) != hipSuccess)
+                rc = KV_EHIP;
+            else
+                ix->ev_used[k] = true;
+        }
+    }
+    if (rc == KV_OK) {
+        ix->full = false;
+        ix->dirty.clear();
     }
     ix->next = k ^ 1;
     if (prev != ix->device) (void)hipSetDevice(prev);
@@ -107,6 +158,7 @@ void release(kv_index *ix) {
             (void)hipEventDestroy(ix->ev[k]);
         }
         if (ix->snap[k]) (void)hipHostFree(ix->snap[k]);
+        if (ix->dev_upd[k]) (void)hipFree(ix->dev_upd[k]);
     }
     if (ix->dev) (void)hipFree(ix->dev);
     delete ix;
@@ -134,7 +186,13 @@ int kv_index_create(int64_t max_entries, kv_index **out) {
     ix->cap = int64_t(1) << ix->log2cap;
     ix->host.assign(ix->cap, IndexEntry{0, -1, kEmpty});
     const size_t bytes = sizeof(IndexEntry) * (size_t)ix->cap;
+    // an incremental upload fits a snapshot buffer (cap entries = cap/2 pairs); past an eighth of the
+    // table, or 65536 pairs, the whole image is sent instead
+    ix->upd_cap = std::min<int64_t>(ix->cap / 8, 65536);
+    const size_t upd_bytes = sizeof(IndexUpdate) * (size_t)ix->upd_cap;
     if (hipGetDevice(&ix->device) != hipSuccess || hipMalloc((void **)&ix->dev, bytes) != hipSuccess ||
+        hipMalloc((void **)&ix->dev_upd[0], upd_bytes) != hipSuccess ||
+        hipMalloc((void **)&ix->dev_upd[1], upd_bytes) != hipSuccess ||
         hipMemset(ix->dev, 0, bytes) != hipSuccess ||
         hipHostMalloc((void **)&ix->snap[0], bytes, hipHostMallocDefault) != hipSuccess ||
         hipHostMalloc((void **)&ix->snap[1], bytes, hipHostMallocDefault) != hipSuccess ||
@@ -164,6 +222,7 @@ int kv_index_insert(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slot
         const int64_t at = probe(idx, h_keys[i], &free_pos);
         if (at >= 0) {
             idx->host[at].slot = h_slots[i];
+            idx->dirty.push_back(at);
             continue;
         }
         if (idx->live >= idx->max_entries || free_pos < 0) {
@@ -172,6 +231,7 @@ int kv_index_insert(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slot
         }
         if (idx->host[free_pos].state == kTomb) --idx->tombs;
         idx->host[free_pos] = IndexEntry{h_keys[i], h_slots[i], kLive};
+        idx->dirty.push_back(free_pos);
         ++idx->live;
         if ((idx->live + idx->tombs) * 4 > idx->cap * 3) rehash(idx);
     }
@@ -186,6 +246,7 @@ int kv_index_erase(kv_index *idx, const uint64_t *h_keys, int32_t n, void *strea
         if (at < 0) continue;
         idx->host[at].state = kTomb;
         idx->host[at].slot = -1;
+        idx->dirty.push_back(at);
         --idx->live;
         ++idx->tombs;
     }

@@ -281,6 +281,44 @@ def test_index_insert_erase_churn():
     idx.destroy()
 
 
+def test_index_updates_small_and_large_batches():
+    # The device table follows the host table through incremental updates (few
+    # changed entries) and whole-table uploads (many changes, rehash); batch
+    # sizes straddle the incremental limit (an eighth of the table).
+    rng = np.random.default_rng(21)
+    toks = rng.integers(0, 32000, 16 * 9000).astype(np.int32)
+    tok_off = np.array([0, toks.size], np.int64)
+    bh = oracle.hash_prefix(toks, tok_off)
+    blk_off = oracle.block_offsets(tok_off)
+    keys = bh.copy()
+    cap_entries = 4096                      # table of 8192 positions: incremental up to 1024 changes
+    idx = kv.KvIndex(cap_entries)
+    ref = {}
+    for it, n in enumerate([1, 10, 1023, 1024, 1025, 3000, 5, 2000, 700, 1, 4096]):
+        cand = {int(keys[i]): int(rng.integers(0, 1 << 20)) for i in rng.choice(keys.size, n, replace=False)}
+        room = cap_entries - len(ref)
+        items = [(k, v) for k, v in cand.items() if k in ref] + \
+                [(k, v) for k, v in cand.items() if k not in ref][:max(room, 0)]
+        if items:
+            idx.insert(np.array([k for k, _ in items], np.uint64), np.array([v for _, v in items], np.int32))
+            ref.update(items)
+        cs, hit = _lookup_gpu(idx, bh, blk_off, 1)
+        ocs, ohit = oracle.lookup(ref, bh, blk_off, 1)
+        assert np.array_equal(cs, ocs) and np.array_equal(hit, ohit), ("insert", it, n)
+        live = list(ref.keys())
+        m = min(len(live), [0, 3, 500, 1024, 1100, 2500][it % 6])
+        gone = [live[i] for i in rng.choice(len(live), m, replace=False)] if m else []
+        if gone:
+            idx.erase(np.array(gone, np.uint64))
+            for k in gone:
+                ref.pop(k)
+        cs, hit = _lookup_gpu(idx, bh, blk_off, 1)
+        ocs, ohit = oracle.lookup(ref, bh, blk_off, 1)
+        assert np.array_equal(cs, ocs) and np.array_equal(hit, ohit), ("erase", it, m)
+        assert idx.size() == len(ref)
+    idx.destroy()
+
+
 def test_out_of_range_jobs_are_skipped_on_device():
     shape = W.KVShape(2, 2, 64, 2, 16, 64)
     w = W.small_random(21, shape, num_reqs=4, max_len=256)
