@@ -203,6 +203,16 @@ int kv_retrieve_scatter(const kv_layout *layout, const void *d_staging, void *co
                         const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
                         const kv_job *d_jobs, int32_t num_jobs, void *stream);
 
+/* The same retrieve for job lists in which each staged chunk is read by at
+ * most one job (no shared prefix among them, e.g. one request's own chunks):
+ * the staged chunks are streamed with non-temporal loads by 1024-lane
+ * workgroups, all loads of a workgroup before its stores.  Any job list gives
+ * the same result as kv_retrieve_scatter; lists that share chunks are slower
+ * this way.  Same arguments, checks and errors. */
+int kv_retrieve_scatter_stream(const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
+                               const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
+                               const kv_job *d_jobs, int32_t num_jobs, void *stream);
+
 /* Store (retaining the KV of complete chunks, Section 5 "Workload"): the
  * inverse walk, paged blocks of (req, chunk) -> staging slot.  Slots must be
  * disjoint within one call.  Same arguments, checks and errors. */

@@ -30,7 +30,7 @@ HASH_BLOCK_TOKENS = 16
 EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
            "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
            "kv_store_gather", "kv_group_jobs_by_slot", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
-           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out", "kv_pipeline_create", "kv_commit_should_stage_n",
+           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out", "kv_pipeline_create", "kv_commit_should_stage_n", "kv_retrieve_scatter_stream",
            "kv_pipeline_destroy", "kv_retrieve_pipelined"]
 
 
@@ -93,6 +93,7 @@ def lib() -> ct.CDLL:
                           ct.POINTER(_i32), ct.POINTER(_i32)],
         "kv_retrieve_scatter": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
         "kv_store_gather": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
+        "kv_retrieve_scatter_stream": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
         "kv_group_jobs_by_slot": [_vp, _i32],
         "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
         "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
@@ -309,6 +310,18 @@ def kv_retrieve_scatter(layout: KvLayout, d_staging, layers: Sequence, d_block_t
                                      _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
                                      _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
                                      _stream(stream)), "kv_retrieve_scatter")
+
+
+def kv_retrieve_scatter_stream(layout: KvLayout, d_staging, layers: Sequence, d_block_tables, bt_stride: int,
+                               num_reqs: int, d_jobs, num_jobs: int, stream=None) -> None:
+    """kv_retrieve_scatter for job lists that read each staged chunk once."""
+    import torch
+    if len(layers) != layout.num_layers:
+        raise ValueError("one paged tensor per layer is required")
+    _check(lib().kv_retrieve_scatter_stream(ct.byref(layout), _dptr(d_staging, None, "staging"), _layer_array(layers),
+                                            _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
+                                            _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
+                                            _stream(stream)), "kv_retrieve_scatter_stream")
 
 
 def kv_store_gather(layout: KvLayout, d_staging, layers: Sequence, d_block_tables, bt_stride: int,

@@ -110,7 +110,17 @@ int kv_retrieve_scatter(const kv_layout *layout, const void *d_staging, void *co
     const int rc = make_copy_params(p, layout, d_staging, (const void *const *)h_layer_ptrs, d_block_tables,
                                     bt_stride, num_reqs, d_jobs, num_jobs);
     if (rc != KV_OK) return rc;
-    return tkv::launch_copy(p, true, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
+    return tkv::launch_copy(p, tkv::kRetrieve, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
+}
+
+int kv_retrieve_scatter_stream(const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
+                               const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
+                               const kv_job *d_jobs, int32_t num_jobs, void *stream) {
+    tkv::CopyParams p;
+    const int rc = make_copy_params(p, layout, d_staging, (const void *const *)h_layer_ptrs, d_block_tables,
+                                    bt_stride, num_reqs, d_jobs, num_jobs);
+    if (rc != KV_OK) return rc;
+    return tkv::launch_copy(p, tkv::kRetrieveStream, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
 }
 
 int kv_store_gather(const kv_layout *layout, void *d_staging, const void *const *h_layer_ptrs,
@@ -120,7 +130,7 @@ int kv_store_gather(const kv_layout *layout, void *d_staging, const void *const 
     const int rc = make_copy_params(p, layout, d_staging, h_layer_ptrs, d_block_tables, bt_stride, num_reqs,
                                     d_jobs, num_jobs);
     if (rc != KV_OK) return rc;
-    return tkv::launch_copy(p, false, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
+    return tkv::launch_copy(p, tkv::kStore, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
 }
 
 int kv_build_jobs(const int32_t *h_hit_chunks, const int32_t *h_chunk_slot, const uint64_t *h_block_hash,

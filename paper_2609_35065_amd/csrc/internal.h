@@ -48,8 +48,15 @@ struct CopyParams {
     int32_t num_jobs;
 };
 
+// Which copy a launch performs.  The two retrieve kinds move the same bytes:
+// kRetrieve reads each staged unit through the caches, for job lists where
+// jobs share staged chunks; kRetrieveStream streams them with non-temporal
+// loads in the store's workgroup shape, for job lists that read each chunk
+// once.
+enum CopyKind { kRetrieve, kRetrieveStream, kStore };
+
 // Launchers (copy.hip, hash.hip).  Return hipSuccess or the launch error.
-hipError_t launch_copy(const CopyParams &p, bool retrieve, hipStream_t stream);
+hipError_t launch_copy(const CopyParams &p, CopyKind kind, hipStream_t stream);
 hipError_t launch_hash(const int32_t *tokens, const int64_t *tok_off, int32_t num_reqs, uint64_t seed,
                        const int64_t *blk_off, uint64_t *out, hipStream_t stream);
 hipError_t launch_lookup(const IndexEntry *table, int log2cap, const uint64_t *block_hash,

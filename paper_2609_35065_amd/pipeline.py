@@ -33,7 +33,7 @@ import torch
 
 from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, KvPipeline, kv_build_jobs, kv_commit_should_stage_n,
                kv_group_jobs_by_slot, kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_pipelined,
-               kv_retrieve_scatter, kv_stage_out, kv_store_gather, make_layout)
+               kv_retrieve_scatter, kv_retrieve_scatter_stream, kv_stage_out, kv_store_gather, make_layout)
 
 LOWER_TIER_MODES = ("zero-copy", "pipelined", "serialized")
 
@@ -290,8 +290,10 @@ class StagingPath:
                 self.d_store[:ns].copy_(self.h_store[:ns], non_blocking=True)
             self._uploaded[par].record(self.stream)
             e = self._ev(timers, "retrieve")
-            kv_retrieve_scatter(self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_retr,
-                                nres, self.stream)
+            # jobs that read distinct staged chunks stream them; shared chunks go through the caches
+            distinct = nres == 0 or np.unique(self.h_retr.numpy()[:nres, 0]).size == nres
+            (kv_retrieve_scatter_stream if distinct else kv_retrieve_scatter)(
+                self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_retr, nres, self.stream)
             if nres < nr:
                 h_jobs = self.h_retr.numpy()[nres:nr]
                 es = None

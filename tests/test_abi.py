@@ -150,7 +150,7 @@ def test_copy_calls_reject_bad_layouts_before_any_launch(over, code):
     lo = _layout(**over)
     L = kv.lib()
     layers = (ct.c_void_p * 128)(*([0x10000] * 128))
-    for f in (L.kv_retrieve_scatter, L.kv_store_gather):
+    for f in (L.kv_retrieve_scatter, L.kv_retrieve_scatter_stream, L.kv_store_gather):
         assert f(ct.byref(lo), 0x10000, layers, 0x10000, 10, 2, 0x10000, 1, None) == code
 
 
@@ -158,7 +158,7 @@ def test_copy_calls_reject_bad_pointers_before_any_launch():
     lo = _layout()
     L = kv.lib()
     good = (ct.c_void_p * 2)(0x10000, 0x20000)
-    for f in (L.kv_retrieve_scatter, L.kv_store_gather):
+    for f in (L.kv_retrieve_scatter, L.kv_retrieve_scatter_stream, L.kv_store_gather):
         assert f(ct.byref(lo), None, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EINVAL
         assert f(ct.byref(lo), 0x10008, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EALIGN
         assert f(ct.byref(lo), 0x10000, (ct.c_void_p * 2)(0x10000, 0x20004), 0x10000, 10, 2, 0x10000, 1,

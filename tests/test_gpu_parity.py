@@ -334,10 +334,37 @@ def test_out_of_range_jobs_are_skipped_on_device():
     oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs)
     kv.kv_store_gather(g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs, d_jobs, len(jobs))
     oracle.store_gather(o.layout, o.staging, o.layers, bt, jobs)
+    jobs2 = jobs.copy()
+    jobs2[-1, 0] = 2
+    kv.kv_retrieve_scatter_stream(g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs,
+                                  torch.from_numpy(jobs2).cuda(), len(jobs2))
+    oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs2)
     torch.cuda.synchronize()
     assert np.array_equal(g.staging.cpu().numpy(), o.staging)
     for l in range(2):
         assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
+
+
+@pytest.mark.parametrize("layout,pad", [("kv_first", 0), ("block_first", 48)])
+@pytest.mark.parametrize("si", range(len(SHAPES)))
+@pytest.mark.parametrize("shared", [False, True])
+def test_streaming_retrieve_matches_oracle(si, layout, pad, shared):
+    # The streaming retrieve is meant for job lists that read each staged
+    # chunk once, and must give the oracle's bytes for any job list.
+    shape = SHAPES[si]
+    w = W.small_random(300 + si, shape, num_reqs=9, max_len=5 * shape.chunk_tokens + 37, paged_layout=layout,
+                       block_pad=pad)
+    g, o = _pair(w)
+    jobs = W.random_retrieve_jobs(w, 300 + si, slots_used=4 if shared else w.num_slots)
+    if not shared:
+        jobs[:, 0] = np.arange(len(jobs)) % w.num_slots          # distinct slots while they last
+    d_jobs = torch.from_numpy(jobs).cuda() if len(jobs) else torch.zeros((1, 4), dtype=torch.int32, device="cuda")
+    kv.kv_retrieve_scatter_stream(g.layout, g.staging, g.layers, g.bt, w.bt_stride, w.num_reqs, d_jobs, len(jobs))
+    oracle.retrieve_scatter(o.layout, o.staging, o.layers, w.block_tables, jobs)
+    torch.cuda.synchronize()
+    for l in range(len(g.layers)):
+        assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l]), f"layer {l} differs"
+    _free(g, o)
 
 
 def test_zero_jobs_enqueue_nothing():
