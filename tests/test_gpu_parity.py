@@ -147,6 +147,22 @@ def test_random_workloads(si, layout, pad):
     _free(g, o)
 
 
+@pytest.mark.parametrize("k", range(40))
+def test_random_shape_sweep(k):
+    # Forty seeded shapes (layers, heads, head size, element size, block and chunk sizes drawn at random),
+    # random paged layout and padding; two passes each, every byte compared.
+    shape = W.random_shapes(2026, 40)[k]
+    layout = "kv_first" if k % 2 == 0 else "block_first"
+    pad = [0, 16, 4096, 48][k % 4]
+    w = W.small_random(700 + k, shape, num_reqs=6, max_len=4 * shape.chunk_tokens + 23, paged_layout=layout,
+                       block_pad=pad)
+    g, o = _pair(w)
+    for p in range(2):
+        sg, so = g.run_pass(validate=True), o.run_pass()
+        _compare_pass(g, o, sg, so)
+    _free(g, o)
+
+
 def test_raw_bit_patterns_nan_payloads():
     shape = W.KVShape(2, 2, 64, 2, 16, 64)
     w = W.small_random(7, shape, num_reqs=6, max_len=300)

@@ -109,3 +109,13 @@ def test_fill_formula_high_words():
     a = W.kv_words_np(1, 1, (1 << 32) + 5, 4)
     b = W.kv_words_np(1, 1, 5, 4)
     assert not np.array_equal(a, b)
+
+
+def test_random_shapes_respect_the_layout_rules():
+    shapes = W.random_shapes(2026, 40)
+    assert len(shapes) == 40 and len(set(shapes)) > 30
+    for sh in shapes:
+        assert sh.chunk_tokens % 16 == 0 and sh.chunk_tokens % sh.block_size == 0
+        assert sh.seg_bytes % 16 == 0
+    assert W.random_shapes(2026, 40) == shapes                      # seeded
+    assert {sh.elem_bytes for sh in shapes} == {1, 2, 4}

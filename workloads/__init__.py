@@ -37,7 +37,7 @@ M32 = 0xFFFFFFFF
 FINITE_MASK = 0xBFFFBFFF   # clears bit 14 of each 16-bit half: no Inf/NaN in fp16 or bf16
 
 # purposes for numpy sub-seeds
-_P_TOK, _P_LEN, _P_ZIPF, _P_PERM, _P_PERM2, _P_SMALL, _P_JOBS = range(7)
+_P_TOK, _P_LEN, _P_ZIPF, _P_PERM, _P_PERM2, _P_SMALL, _P_JOBS, _P_SHAPES = range(8)
 
 
 # --------------------------------------------------------------------------
@@ -362,6 +362,25 @@ def repermute_block_tables(w: Workload, purpose_salt: int = 0) -> None:
         bt[r, :need[r]] = perm[pos:pos + need[r]]
         pos += int(need[r])
     w.block_tables = bt
+
+
+def random_shapes(seed: int, n: int) -> List[KVShape]:
+    """n KV shapes for parity sweeps: 1-6 layers, 1-8 KV heads, head sizes 16-128 (80 and 96 included),
+    1/2/4-byte elements, blocks of 1-32 tokens, chunks of 1-8 blocks; the chunk is a whole number of 16-token
+    hash blocks and a paged segment a whole number of 16-byte vectors."""
+    rng = _rng(seed, _P_SHAPES)
+    out: List[KVShape] = []
+    while len(out) < n:
+        L = int(rng.integers(1, 7))
+        H = int(rng.choice([1, 2, 3, 4, 8]))
+        D = int(rng.choice([16, 32, 64, 80, 96, 128]))
+        e = int(rng.choice([1, 2, 4]))
+        B = int(rng.choice([1, 2, 4, 8, 16, 32]))
+        C = int(B * rng.choice([1, 2, 4, 8]))
+        if C % 16 or (B * H * D * e) % 16:
+            continue
+        out.append(KVShape(L, H, D, e, B, C))
+    return out
 
 
 def random_retrieve_jobs(w: Workload, seed: int, slots_used: int) -> np.ndarray:
