@@ -423,7 +423,8 @@ def main() -> int:
                    "chunk_tokens": w.shape.chunk_tokens, "requests": w.num_reqs, "tokens": n_tok,
                    "pool_blocks": w.num_blocks, "staging_slots": w.num_slots,
                    "retrieve_jobs": stats.num_retrieve, "store_jobs": stats.num_store,
-                   "steps_overlap": not args.serial},
+                   "steps_overlap": not args.serial,
+                   "retrieve_variant": {0: "unit", 1: "pair", 2: "stream"}.get(path.retrieve_kind)},
         "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic},
         "kernels": {

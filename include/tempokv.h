@@ -10,7 +10,8 @@
  *   kv_hash_prefix        chained 64-bit hash of token ids over 16-token blocks
  *   kv_lookup             prefix match of chunk keys against a staged-chunk index
  *   kv_build_jobs         host job build: hits -> retrieve jobs, misses -> store jobs
- *   kv_retrieve_scatter   staged chunk [L,2,C,H,D] -> paged KV blocks (one launch)
+ *   kv_retrieve_scatter   staged chunk [L,2,C,H,D] -> paged KV blocks (one launch;
+ *                         kv_retrieve_plan / kv_retrieve_scatter_as pick a variant)
  *   kv_store_gather       paged KV blocks -> staged chunk (one launch)
  *   kv_commit_should_stage  the TTU/TTR commitment rule of Section 3.2 (host)
  *   kv_stage_in / kv_retrieve_pipelined  lower tier -> HBM staging, and the
@@ -203,15 +204,32 @@ int kv_retrieve_scatter(const kv_layout *layout, const void *d_staging, void *co
                         const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
                         const kv_job *d_jobs, int32_t num_jobs, void *stream);
 
-/* The same retrieve for job lists in which each staged chunk is read by at
- * most one job (no shared prefix among them, e.g. one request's own chunks):
- * the staged chunks are streamed with non-temporal loads by 1024-lane
- * workgroups, all loads of a workgroup before its stores.  Any job list gives
- * the same result as kv_retrieve_scatter; lists that share chunks are slower
- * this way.  Same arguments, checks and errors. */
-int kv_retrieve_scatter_stream(const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
-                               const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
-                               const kv_job *d_jobs, int32_t num_jobs, void *stream);
+/* Variants of the retrieve.  All give the bytes of kv_retrieve_scatter for
+ * any job list; they differ in speed by the way jobs share staged chunks. */
+typedef enum kv_retrieve_kind {
+    KV_RETRIEVE_UNIT = 0,   /* one workgroup per (job, layer, plane) unit; jobs that share a chunk read it
+                               through the L2 (kv_retrieve_scatter) */
+    KV_RETRIEVE_PAIR = 1,   /* one workgroup per pair of consecutive jobs: a pair naming one chunk reads each
+                               stage once and writes it twice (32 KiB segments; other sizes use UNIT) */
+    KV_RETRIEVE_STREAM = 2  /* 1024-lane workgroups, non-temporal loads of the staged chunks: for lists that
+                               read each chunk once */
+} kv_retrieve_kind;
+
+/* Pick the variant for a job list from its host copy (grouped by slot, as
+ * kv_group_jobs_by_slot leaves it): STREAM when every slot appears once; PAIR
+ * when the segments are 32 KiB, at least 90 % of the job pairs (0,1), (2,3),
+ * ... name one slot and the groups of equal slots average at most 16 jobs;
+ * UNIT otherwise.  The thresholds are measured (lists with groups of 8, as in
+ * a batch whose requests share a handful of prefixes, gain 3-13 % from PAIR;
+ * irregular or very large groups lose 1-3 %).  Returns a kv_retrieve_kind, or
+ * KV_EINVAL / a layout error. */
+int kv_retrieve_plan(const kv_layout *layout, const kv_job *h_jobs, int32_t num_jobs);
+
+/* kv_retrieve_scatter with an explicit variant (a kv_retrieve_kind).  Same
+ * arguments, checks and errors, plus KV_EINVAL for an unknown kind. */
+int kv_retrieve_scatter_as(int32_t kind, const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
+                           const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
+                           const kv_job *d_jobs, int32_t num_jobs, void *stream);
 
 /* Store (retaining the KV of complete chunks, Section 5 "Workload"): the
  * inverse walk, paged blocks of (req, chunk) -> staging slot.  Slots must be

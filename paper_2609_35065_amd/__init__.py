@@ -21,6 +21,7 @@ LIB_PATH = os.path.join(_HERE, "libtempokv.so")
 KV_OK, KV_EINVAL, KV_EALIGN, KV_ERANGE, KV_ENOSPC, KV_EHIP, KV_EDUP = 0, -1, -2, -3, -4, -5, -6
 KV_DEFER, KV_COMMIT, KV_BLOCKED, KV_ORDINARY = 0, 1, 2, 3
 KV_POLICY_DEMAND, KV_POLICY_IMMEDIATE, KV_POLICY_QUEUE_K, KV_POLICY_TEMPO_STATIC, KV_POLICY_TEMPO = range(5)
+KV_RETRIEVE_UNIT, KV_RETRIEVE_PAIR, KV_RETRIEVE_STREAM = range(3)
 SIM_TRACE_KINDS = ["arrive", "admit", "commit", "ordinary", "ready", "stageready", "transfer", "fetch", "release",
                    "done", "evict"]
 KV_MAX_LAYERS = 128
@@ -30,7 +31,8 @@ HASH_BLOCK_TOKENS = 16
 EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
            "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
            "kv_store_gather", "kv_group_jobs_by_slot", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
-           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out", "kv_pipeline_create", "kv_commit_should_stage_n", "kv_retrieve_scatter_stream",
+           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out", "kv_pipeline_create", "kv_commit_should_stage_n", "kv_retrieve_plan",
+           "kv_retrieve_scatter_as",
            "kv_pipeline_destroy", "kv_retrieve_pipelined"]
 
 
@@ -93,7 +95,8 @@ def lib() -> ct.CDLL:
                           ct.POINTER(_i32), ct.POINTER(_i32)],
         "kv_retrieve_scatter": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
         "kv_store_gather": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
-        "kv_retrieve_scatter_stream": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
+        "kv_retrieve_plan": [ct.POINTER(KvLayout), _vp, _i32],
+        "kv_retrieve_scatter_as": [_i32, ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
         "kv_group_jobs_by_slot": [_vp, _i32],
         "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
         "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
@@ -312,16 +315,23 @@ def kv_retrieve_scatter(layout: KvLayout, d_staging, layers: Sequence, d_block_t
                                      _stream(stream)), "kv_retrieve_scatter")
 
 
-def kv_retrieve_scatter_stream(layout: KvLayout, d_staging, layers: Sequence, d_block_tables, bt_stride: int,
-                               num_reqs: int, d_jobs, num_jobs: int, stream=None) -> None:
-    """kv_retrieve_scatter for job lists that read each staged chunk once."""
+def kv_retrieve_plan(layout: KvLayout, h_jobs: np.ndarray) -> int:
+    """The retrieve variant (KV_RETRIEVE_*) for a job list ([n,4] int32, grouped by slot)."""
+    hj = np.ascontiguousarray(h_jobs, np.int32).reshape(-1, 4)
+    return _check(lib().kv_retrieve_plan(ct.byref(layout), hj.ctypes.data if hj.size else None, hj.shape[0]),
+                  "kv_retrieve_plan")
+
+
+def kv_retrieve_scatter_as(kind: int, layout: KvLayout, d_staging, layers: Sequence, d_block_tables,
+                           bt_stride: int, num_reqs: int, d_jobs, num_jobs: int, stream=None) -> None:
+    """kv_retrieve_scatter with an explicit variant (KV_RETRIEVE_UNIT / PAIR / STREAM)."""
     import torch
     if len(layers) != layout.num_layers:
         raise ValueError("one paged tensor per layer is required")
-    _check(lib().kv_retrieve_scatter_stream(ct.byref(layout), _dptr(d_staging, None, "staging"), _layer_array(layers),
-                                            _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
-                                            _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
-                                            _stream(stream)), "kv_retrieve_scatter_stream")
+    _check(lib().kv_retrieve_scatter_as(kind, ct.byref(layout), _dptr(d_staging, None, "staging"),
+                                        _layer_array(layers), _dptr(d_block_tables, torch.int32, "block_tables"),
+                                        bt_stride, num_reqs, _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None,
+                                        num_jobs, _stream(stream)), "kv_retrieve_scatter_as")
 
 
 def kv_store_gather(layout: KvLayout, d_staging, layers: Sequence, d_block_tables, bt_stride: int,

@@ -113,14 +113,47 @@ int kv_retrieve_scatter(const kv_layout *layout, const void *d_staging, void *co
     return tkv::launch_copy(p, tkv::kRetrieve, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
 }
 
-int kv_retrieve_scatter_stream(const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
-                               const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
-                               const kv_job *d_jobs, int32_t num_jobs, void *stream) {
+int kv_retrieve_plan(const kv_layout *layout, const kv_job *h_jobs, int32_t num_jobs) {
+    const int rc = check_layout(layout);
+    if (rc != KV_OK) return rc;
+    if (num_jobs < 0 || (num_jobs > 0 && !h_jobs)) return KV_EINVAL;
+    if (num_jobs == 0) return KV_RETRIEVE_UNIT;
+    int64_t runs = 0, pairs_shared = 0;
+    for (int32_t i = 0; i < num_jobs; ++i) {
+        if (i == 0 || h_jobs[i].slot != h_jobs[i - 1].slot) ++runs;
+        if ((i & 1) && h_jobs[i].slot == h_jobs[i - 1].slot) ++pairs_shared;
+    }
+    if (runs == num_jobs) {
+        // no slot twice in a row; streaming needs every slot once
+        std::unordered_set<int32_t> seen;
+        seen.reserve((size_t)num_jobs * 2);
+        bool distinct = true;
+        for (int32_t i = 0; i < num_jobs && distinct; ++i) distinct = seen.insert(h_jobs[i].slot).second;
+        if (distinct) return KV_RETRIEVE_STREAM;
+    }
+    // Pairs pay off when most pairs share their chunk and groups are small
+    // (many groups in flight per XCD); measured at 32 KiB segments.
+    const int64_t seg = (int64_t)layout->block_size * layout->kv_heads * layout->head_dim * layout->elem_bytes;
+    if (seg == 32768 && 20 * pairs_shared >= 9 * (int64_t)num_jobs && num_jobs <= 16 * runs)
+        return KV_RETRIEVE_PAIR;
+    return KV_RETRIEVE_UNIT;
+}
+
+int kv_retrieve_scatter_as(int32_t kind, const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
+                           const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs, const kv_job *d_jobs,
+                           int32_t num_jobs, void *stream) {
+    tkv::CopyKind k;
+    switch (kind) {
+    case KV_RETRIEVE_UNIT: k = tkv::kRetrieve; break;
+    case KV_RETRIEVE_PAIR: k = tkv::kRetrievePair; break;
+    case KV_RETRIEVE_STREAM: k = tkv::kRetrieveStream; break;
+    default: return KV_EINVAL;
+    }
     tkv::CopyParams p;
     const int rc = make_copy_params(p, layout, d_staging, (const void *const *)h_layer_ptrs, d_block_tables,
                                     bt_stride, num_reqs, d_jobs, num_jobs);
     if (rc != KV_OK) return rc;
-    return tkv::launch_copy(p, tkv::kRetrieveStream, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
+    return tkv::launch_copy(p, k, (hipStream_t)stream) == hipSuccess ? KV_OK : KV_EHIP;
 }
 
 int kv_store_gather(const kv_layout *layout, void *d_staging, const void *const *h_layer_ptrs,

@@ -48,12 +48,13 @@ struct CopyParams {
     int32_t num_jobs;
 };
 
-// Which copy a launch performs.  The two retrieve kinds move the same bytes:
-// kRetrieve reads each staged unit through the caches, for job lists where
-// jobs share staged chunks; kRetrieveStream streams them with non-temporal
-// loads in the store's workgroup shape, for job lists that read each chunk
-// once.
-enum CopyKind { kRetrieve, kRetrieveStream, kStore };
+// Which copy a launch performs.  The retrieve kinds move the same bytes:
+// kRetrieve walks one (job, layer, plane) unit per workgroup, reading staged
+// units through the caches; kRetrievePair walks pairs of jobs and reads a
+// unit once for two jobs that share it; kRetrieveStream streams the staged
+// units with non-temporal loads in the store's workgroup shape, for job lists
+// that read each chunk once.
+enum CopyKind { kRetrieve, kRetrievePair, kRetrieveStream, kStore };
 
 // Launchers (copy.hip, hash.hip).  Return hipSuccess or the launch error.
 hipError_t launch_copy(const CopyParams &p, CopyKind kind, hipStream_t stream);

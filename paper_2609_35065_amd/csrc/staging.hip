@@ -137,8 +137,7 @@ int kv_retrieve_pipelined(kv_pipeline *pl, const kv_layout *layout, const void *
             }
             ++q1;
         }
-        // a batch whose jobs read distinct slots streams them; shared slots go through the caches
-        const bool distinct = (int64_t)slots.size() == q1 - q0;
+        const int kind = kv_retrieve_plan(layout, h_jobs + q0, q1 - q0);
         std::sort(slots.begin(), slots.end());
         slots.erase(std::unique(slots.begin(), slots.end()), slots.end());
         rc = copy_slots(layout, (char *)d_staging, (const char *)h_lower_tier, slots.data(), (int32_t)slots.size(),
@@ -151,9 +150,10 @@ int kv_retrieve_pipelined(kv_pipeline *pl, const kv_layout *layout, const void *
         pb.jobs = d_jobs + q0;
         pb.num_jobs = q1 - q0;
         pb.total_segs = (int64_t)pb.num_jobs * p.L * 2 * p.nseg;
-        if (tkv::launch_copy(pb, distinct ? tkv::kRetrieveStream : tkv::kRetrieve, (hipStream_t)stream) !=
-            hipSuccess)
-            return KV_EHIP;
+        const tkv::CopyKind ck = kind == KV_RETRIEVE_STREAM ? tkv::kRetrieveStream
+                                 : kind == KV_RETRIEVE_PAIR ? tkv::kRetrievePair
+                                                            : tkv::kRetrieve;
+        if (tkv::launch_copy(pb, ck, (hipStream_t)stream) != hipSuccess) return KV_EHIP;
         q0 = q1;
     }
     return KV_OK;

@@ -3,7 +3,8 @@
 A pass is:  hash (kv_hash_prefix) -> lookup (kv_lookup) -> one device-to-host
 copy of the lookup result -> host job build (kv_build_jobs) and commitment
 decisions (kv_commit_should_stage_n) -> one host-to-device copy of the jobs ->
-retrieve scatter (kv_retrieve_scatter) -> store gather (kv_store_gather) ->
+retrieve scatter (kv_retrieve_plan picks the copy variant, kv_retrieve_scatter_as
+runs it) -> store gather (kv_store_gather) ->
 index update (kv_index_insert; optionally kv_index_erase of what was just
 stored, which returns the batch to its starting state so that passes can be
 repeated).
@@ -33,7 +34,7 @@ import torch
 
 from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, KvPipeline, kv_build_jobs, kv_commit_should_stage_n,
                kv_group_jobs_by_slot, kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_pipelined,
-               kv_retrieve_scatter, kv_retrieve_scatter_stream, kv_stage_out, kv_store_gather, make_layout)
+               kv_retrieve_plan, kv_retrieve_scatter_as, kv_stage_out, kv_store_gather, make_layout)
 
 LOWER_TIER_MODES = ("zero-copy", "pipelined", "serialized")
 
@@ -104,6 +105,7 @@ class StagingPath:
         self.last_store_slots = np.zeros(0, np.int32)
         self.last_retrieve = np.zeros((0, 4), np.int32)
         self.last_store = np.zeros((0, 4), np.int32)
+        self.retrieve_kind: Optional[int] = None
 
     def set_batch(self, w) -> None:
         """Load a new request batch (tokens, offsets, block tables) that uses
@@ -290,10 +292,10 @@ class StagingPath:
                 self.d_store[:ns].copy_(self.h_store[:ns], non_blocking=True)
             self._uploaded[par].record(self.stream)
             e = self._ev(timers, "retrieve")
-            # jobs that read distinct staged chunks stream them; shared chunks go through the caches
-            distinct = nres == 0 or np.unique(self.h_retr.numpy()[:nres, 0]).size == nres
-            (kv_retrieve_scatter_stream if distinct else kv_retrieve_scatter)(
-                self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_retr, nres, self.stream)
+            # the copy variant suited to how these jobs share staged chunks
+            self.retrieve_kind = kv_retrieve_plan(self.layout, self.h_retr.numpy()[:nres])
+            kv_retrieve_scatter_as(self.retrieve_kind, self.layout, self.staging_ptr, self.layers, self.bt,
+                                   w.bt_stride, R, self.d_retr, nres, self.stream)
             if nres < nr:
                 h_jobs = self.h_retr.numpy()[nres:nr]
                 es = None

@@ -140,6 +140,10 @@ def test_validate_jobs():
     assert kv.kv_validate_jobs(lo, bt2, ok, True) == kv.KV_ERANGE
 
 
+def _as(L, kind):
+    return lambda *args: L.kv_retrieve_scatter_as(kind, *args)
+
+
 @pytest.mark.parametrize("over,code", [
     (dict(num_layers=0), kv.KV_EINVAL), (dict(num_layers=129), kv.KV_EINVAL), (dict(elem_bytes=3), kv.KV_EINVAL),
     (dict(chunk_tokens=24), kv.KV_EINVAL), (dict(num_blocks=0), kv.KV_EINVAL), (dict(num_slots=0), kv.KV_EINVAL),
@@ -150,7 +154,7 @@ def test_copy_calls_reject_bad_layouts_before_any_launch(over, code):
     lo = _layout(**over)
     L = kv.lib()
     layers = (ct.c_void_p * 128)(*([0x10000] * 128))
-    for f in (L.kv_retrieve_scatter, L.kv_retrieve_scatter_stream, L.kv_store_gather):
+    for f in (L.kv_retrieve_scatter, _as(L, kv.KV_RETRIEVE_PAIR), _as(L, kv.KV_RETRIEVE_STREAM), L.kv_store_gather):
         assert f(ct.byref(lo), 0x10000, layers, 0x10000, 10, 2, 0x10000, 1, None) == code
 
 
@@ -158,7 +162,8 @@ def test_copy_calls_reject_bad_pointers_before_any_launch():
     lo = _layout()
     L = kv.lib()
     good = (ct.c_void_p * 2)(0x10000, 0x20000)
-    for f in (L.kv_retrieve_scatter, L.kv_retrieve_scatter_stream, L.kv_store_gather):
+    for f in (L.kv_retrieve_scatter, _as(L, kv.KV_RETRIEVE_UNIT), _as(L, kv.KV_RETRIEVE_PAIR),
+              _as(L, kv.KV_RETRIEVE_STREAM), L.kv_store_gather):
         assert f(ct.byref(lo), None, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EINVAL
         assert f(ct.byref(lo), 0x10008, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EALIGN
         assert f(ct.byref(lo), 0x10000, (ct.c_void_p * 2)(0x10000, 0x20004), 0x10000, 10, 2, 0x10000, 1,
@@ -231,3 +236,43 @@ def test_pipeline_calls_check_arguments():
                                    0x10000, 1, 1, None, None) == kv.KV_EINVAL
     assert L.kv_retrieve_pipelined(0x1000, ct.byref(lo), 0x10000, 0x10000, layers, 0x10000, 10, 2,
                                    jobs.ctypes.data, 0x10000, 1, 0, None, None) == kv.KV_EINVAL
+
+
+def _jobs(slots):
+    j = np.zeros((len(slots), 4), np.int32)
+    j[:, 0] = slots
+    j[:, 1] = np.arange(len(slots))
+    return j
+
+
+def test_retrieve_plan_rules():
+    lo32 = kv.make_layout(2, 8, 128, 2, 16, 256, 1000, 700, 1000 * 32768, 32768)     # 32 KiB segments
+    lo4 = kv.make_layout(2, 2, 64, 2, 16, 64, 1000, 700, 1000 * 4096, 4096)          # 4 KiB segments
+    P = kv.kv_retrieve_plan
+    assert P(lo32, np.zeros((0, 4), np.int32)) == kv.KV_RETRIEVE_UNIT
+    assert P(lo32, _jobs(np.arange(100))) == kv.KV_RETRIEVE_STREAM                   # every slot once
+    assert P(lo32, _jobs(np.arange(100)[::-1])) == kv.KV_RETRIEVE_STREAM
+    assert P(lo32, _jobs([0, 1, 0, 1])) == kv.KV_RETRIEVE_UNIT                        # no run, but not distinct
+    groups8 = np.repeat(np.arange(64), 8)                                             # 64 chunks x 8 requests
+    assert P(lo32, _jobs(groups8)) == kv.KV_RETRIEVE_PAIR
+    assert P(lo4, _jobs(groups8)) == kv.KV_RETRIEVE_UNIT                              # pairs only at 32 KiB
+    assert P(lo32, _jobs(np.repeat(np.arange(4), 64))) == kv.KV_RETRIEVE_UNIT         # groups of 64
+    assert P(lo32, _jobs(np.repeat(np.arange(40), 16))) == kv.KV_RETRIEVE_PAIR        # groups of 16
+    odd = np.concatenate([np.repeat(np.arange(50), 3), np.repeat(np.arange(50, 60), 2)])
+    assert P(lo32, _jobs(odd)) == kv.KV_RETRIEVE_UNIT                                 # groups of 3: pairs misalign
+    rng = np.random.default_rng(3)
+    sizes = rng.integers(1, 9, 200)
+    assert P(lo32, _jobs(np.repeat(np.arange(200), sizes))) == kv.KV_RETRIEVE_UNIT    # irregular groups
+    L = kv.lib()
+    assert L.kv_retrieve_plan(None, None, 0) == kv.KV_EINVAL
+    assert L.kv_retrieve_plan(ct.byref(lo32), None, 3) == kv.KV_EINVAL
+    assert L.kv_retrieve_plan(ct.byref(lo32), None, -1) == kv.KV_EINVAL
+
+
+def test_retrieve_as_rejects_unknown_kinds():
+    lo = _layout()
+    L = kv.lib()
+    layers = (ct.c_void_p * 2)(0x10000, 0x20000)
+    for kind in (-1, 3, 99):
+        assert L.kv_retrieve_scatter_as(kind, ct.byref(lo), 0x10000, layers, 0x10000, 10, 2, 0x10000, 1,
+                                        None) == kv.KV_EINVAL

@@ -350,11 +350,12 @@ def test_out_of_range_jobs_are_skipped_on_device():
     oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs)
     kv.kv_store_gather(g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs, d_jobs, len(jobs))
     oracle.store_gather(o.layout, o.staging, o.layers, bt, jobs)
-    jobs2 = jobs.copy()
-    jobs2[-1, 0] = 2
-    kv.kv_retrieve_scatter_stream(g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs,
+    for kind in (kv.KV_RETRIEVE_PAIR, kv.KV_RETRIEVE_STREAM):
+        jobs2 = jobs.copy()
+        jobs2[-1, 0] = 2 + kind
+        kv.kv_retrieve_scatter_as(kind, g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs,
                                   torch.from_numpy(jobs2).cuda(), len(jobs2))
-    oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs2)
+        oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs2)
     torch.cuda.synchronize()
     assert np.array_equal(g.staging.cpu().numpy(), o.staging)
     for l in range(2):
@@ -363,19 +364,29 @@ def test_out_of_range_jobs_are_skipped_on_device():
 
 @pytest.mark.parametrize("layout,pad", [("kv_first", 0), ("block_first", 48)])
 @pytest.mark.parametrize("si", range(len(SHAPES)))
-@pytest.mark.parametrize("shared", [False, True])
-def test_streaming_retrieve_matches_oracle(si, layout, pad, shared):
-    # The streaming retrieve is meant for job lists that read each staged
-    # chunk once, and must give the oracle's bytes for any job list.
+@pytest.mark.parametrize("sharing", ["distinct", "pairs", "mixed"])
+@pytest.mark.parametrize("kind", [1, 2])
+def test_retrieve_variants_match_oracle(kind, sharing, si, layout, pad):
+    # Every variant must give the oracle's bytes for any job list: distinct slots, slots shared by aligned
+    # pairs, and a mixed list (odd length, pairs that straddle two slots, out-of-range jobs in between).
     shape = SHAPES[si]
     w = W.small_random(300 + si, shape, num_reqs=9, max_len=5 * shape.chunk_tokens + 37, paged_layout=layout,
                        block_pad=pad)
     g, o = _pair(w)
-    jobs = W.random_retrieve_jobs(w, 300 + si, slots_used=4 if shared else w.num_slots)
-    if not shared:
-        jobs[:, 0] = np.arange(len(jobs)) % w.num_slots          # distinct slots while they last
-    d_jobs = torch.from_numpy(jobs).cuda() if len(jobs) else torch.zeros((1, 4), dtype=torch.int32, device="cuda")
-    kv.kv_retrieve_scatter_stream(g.layout, g.staging, g.layers, g.bt, w.bt_stride, w.num_reqs, d_jobs, len(jobs))
+    jobs = W.random_retrieve_jobs(w, 300 + si, slots_used=w.num_slots)
+    n = len(jobs)
+    if sharing == "distinct":
+        jobs[:, 0] = np.arange(n) % w.num_slots
+    elif sharing == "pairs":
+        jobs[:, 0] = (np.arange(n) // 2) % w.num_slots
+    else:
+        jobs[:, 0] = (np.arange(n) // 3) % w.num_slots
+        jobs = np.concatenate([jobs[: n - 1 + (n % 2)], [[w.num_slots, 0, 0, 0], [0, w.num_reqs, 0, 0]]])
+        jobs[1::5, 2] = -1                                          # invalid chunk: skipped
+        assert len(jobs) % 2 == 1
+    jobs = np.ascontiguousarray(jobs, np.int32)
+    d_jobs = torch.from_numpy(jobs).cuda()
+    kv.kv_retrieve_scatter_as(kind, g.layout, g.staging, g.layers, g.bt, w.bt_stride, w.num_reqs, d_jobs, len(jobs))
     oracle.retrieve_scatter(o.layout, o.staging, o.layers, w.block_tables, jobs)
     torch.cuda.synchronize()
     for l in range(len(g.layers)):
