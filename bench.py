@@ -9,7 +9,10 @@ again at its end, so every step does the same work).  Inputs (tokens, block
 tables, staging and pool contents) are resident in HBM before timing starts.
 Steps overlap as in a serving loop: the hash and lookup of step i+1 run on a
 stream of their own, and its jobs are built on the host, while the copies of
-step i are in flight (--serial runs them back to back).
+step i are in flight (--serial runs them back to back).  After the warm-up
+steps, and outside the timed region, the retrieve variant for this pool is
+chosen by timing the planned one against the four-job-window one (--no-tune
+keeps the plan).
 
 Prints one JSON line: the whole-step payload rate in GB/s (bytes read plus
 bytes written by the scatter and the gather, divided by wall time per step),
@@ -300,6 +303,8 @@ def main() -> int:
     ap.add_argument("--serial", action="store_true",
                     help="run each step's hash and lookup after the previous step's copies instead of overlapping "
                          "them (with the host job build) with those copies")
+    ap.add_argument("--no-tune", action="store_true",
+                    help="run the planned retrieve variant without timing it against the four-job-window one")
     ap.add_argument("--no-fill", action="store_true",
                     help="leave KV buffers uninitialised (hardware-counter runs: no generator kernels run; the "
                          "copies move the same bytes) and skip the device-copy and CPU-baseline extras")
@@ -318,6 +323,7 @@ def main() -> int:
     import numpy as np
     import torch
     import workloads as W
+    from paper_2609_35065_amd import RETRIEVE_KIND_NAMES
     from paper_2609_35065_amd.pipeline import StagingPath
 
     if not torch.cuda.is_available():
@@ -354,6 +360,8 @@ def main() -> int:
     steps(args.warmup)
     torch.cuda.synchronize()
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+    # pick the retrieve variant for this pool by timing (outside the timed steps)
+    tuning = path.tune_retrieve() if args.warmup and not args.no_tune else {}
 
     timers: dict = {}
     torch.cuda.synchronize()
@@ -424,7 +432,8 @@ def main() -> int:
                    "pool_blocks": w.num_blocks, "staging_slots": w.num_slots,
                    "retrieve_jobs": stats.num_retrieve, "store_jobs": stats.num_store,
                    "steps_overlap": not args.serial,
-                   "retrieve_variant": {0: "unit", 1: "pair", 2: "stream"}.get(path.retrieve_kind)},
+                   "retrieve_variant": RETRIEVE_KIND_NAMES.get(path.retrieve_kind),
+                   "retrieve_tuning_ms": tuning},
         "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic},
         "kernels": {

@@ -211,8 +211,15 @@ typedef enum kv_retrieve_kind {
                                through the L2 (kv_retrieve_scatter) */
     KV_RETRIEVE_PAIR = 1,   /* one workgroup per pair of consecutive jobs: a pair naming one chunk reads each
                                stage once and writes it twice (32 KiB segments; other sizes use UNIT) */
-    KV_RETRIEVE_STREAM = 2  /* 1024-lane workgroups, non-temporal loads of the staged chunks: for lists that
+    KV_RETRIEVE_STREAM = 2, /* 1024-lane workgroups, non-temporal loads of the staged chunks: for lists that
                                read each chunk once */
+    KV_RETRIEVE_QUAD = 3    /* one 1024-lane workgroup per (layer, plane, 4 consecutive jobs, segment): jobs of
+                               the window that share a chunk load it together, one read from memory and the
+                               rest from L2.  Segments of 4, 8, 16, 32 or 64 KiB (other sizes use the generic
+                               copy).  Never returned by kv_retrieve_plan: whether it beats PAIR/UNIT depends on
+                               where the paged pool lies in physical memory (it does on most placements
+                               measured, by about 6 %, and loses where scattered writes run fast), so a caller
+                               picks it by timing both on its own pool. */
 } kv_retrieve_kind;
 
 /* Pick the variant for a job list from its host copy (grouped by slot, as

@@ -21,7 +21,9 @@ LIB_PATH = os.path.join(_HERE, "libtempokv.so")
 KV_OK, KV_EINVAL, KV_EALIGN, KV_ERANGE, KV_ENOSPC, KV_EHIP, KV_EDUP = 0, -1, -2, -3, -4, -5, -6
 KV_DEFER, KV_COMMIT, KV_BLOCKED, KV_ORDINARY = 0, 1, 2, 3
 KV_POLICY_DEMAND, KV_POLICY_IMMEDIATE, KV_POLICY_QUEUE_K, KV_POLICY_TEMPO_STATIC, KV_POLICY_TEMPO = range(5)
-KV_RETRIEVE_UNIT, KV_RETRIEVE_PAIR, KV_RETRIEVE_STREAM = range(3)
+KV_RETRIEVE_UNIT, KV_RETRIEVE_PAIR, KV_RETRIEVE_STREAM, KV_RETRIEVE_QUAD = range(4)
+RETRIEVE_KIND_NAMES = {KV_RETRIEVE_UNIT: "unit", KV_RETRIEVE_PAIR: "pair", KV_RETRIEVE_STREAM: "stream",
+                       KV_RETRIEVE_QUAD: "quad"}
 SIM_TRACE_KINDS = ["arrive", "admit", "commit", "ordinary", "ready", "stageready", "transfer", "fetch", "release",
                    "done", "evict"]
 KV_MAX_LAYERS = 128
@@ -324,7 +326,7 @@ def kv_retrieve_plan(layout: KvLayout, h_jobs: np.ndarray) -> int:
 
 def kv_retrieve_scatter_as(kind: int, layout: KvLayout, d_staging, layers: Sequence, d_block_tables,
                            bt_stride: int, num_reqs: int, d_jobs, num_jobs: int, stream=None) -> None:
-    """kv_retrieve_scatter with an explicit variant (KV_RETRIEVE_UNIT / PAIR / STREAM)."""
+    """kv_retrieve_scatter with an explicit variant (KV_RETRIEVE_UNIT / PAIR / STREAM / QUAD)."""
     import torch
     if len(layers) != layout.num_layers:
         raise ValueError("one paged tensor per layer is required")

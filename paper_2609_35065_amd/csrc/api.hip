@@ -147,6 +147,7 @@ int kv_retrieve_scatter_as(int32_t kind, const kv_layout *layout, const void *d_
     case KV_RETRIEVE_UNIT: k = tkv::kRetrieve; break;
     case KV_RETRIEVE_PAIR: k = tkv::kRetrievePair; break;
     case KV_RETRIEVE_STREAM: k = tkv::kRetrieveStream; break;
+    case KV_RETRIEVE_QUAD: k = tkv::kRetrieveQuad; break;
     default: return KV_EINVAL;
     }
     tkv::CopyParams p;

@@ -33,7 +33,11 @@
 // The pair retrieve walks two consecutive jobs per workgroup and, when they
 // name one staged chunk, loads each stage once for both: with groups of 8
 // requests per chunk it is 3-13 % faster than the unit walk.  The host picks
-// among the three retrieves from the job list (kv_retrieve_plan).
+// among these three retrieves from the job list (kv_retrieve_plan).  A fourth,
+// the four-job-window retrieve (one segment of four consecutive jobs per
+// 1024-lane workgroup), is faster than the pair walk on pools where the memory
+// system takes scattered writes slowly and slower elsewhere, so the caller
+// picks it by timing.
 //
 // On MI355X these shapes were chosen by measurement: at 256 lanes a plain
 // contiguous copy tops out near 5.2 TB/s (read + write), at 1024 lanes near
@@ -230,6 +234,52 @@ __global__ __launch_bounds__(256) void retrieve_pair_kernel(CopyParams p) {
 }
 
 // --------------------------------------------------------------------------
+// Retrieve, windows of four jobs (R rows of 4 KiB per segment): a unit is
+// (layer, plane, window of jobs 4w..4w+3, segment s), copied by one 1024-lane
+// workgroup whose quarter j moves job 4w+j's segment s.  Jobs of a window that
+// share a staged chunk load the same bytes at the same time, so one load comes
+// from memory and the others from L2.  Units are (layer, plane)-major, then
+// groups of kQuadGroup windows (32 jobs), then segment, then window, in plain
+// dispatch order: the workgroups in flight write one segment of 32 jobs at a
+// time.  (Window-major order, and groups of 1, 2 or 4 windows, measured 2-7 %
+// slower.)
+// --------------------------------------------------------------------------
+constexpr int kQuadGroup = 8;
+
+template <int R>
+__global__ __launch_bounds__(1024) void retrieve_quad_kernel(CopyParams p) {
+    constexpr int T = 256;
+    // the quarter is uniform within each 64-lane wave
+    const int j = __builtin_amdgcn_readfirstlane(threadIdx.x >> 8);
+    const int tid = threadIdx.x & (T - 1);
+    const int64_t ngroup = ((int64_t)p.num_jobs + 4 * kQuadGroup - 1) / (4 * kQuadGroup);
+    const int64_t units = ngroup * kQuadGroup * p.nseg * p.L * 2;
+    for (int64_t u = blockIdx.x; u < units; u += gridDim.x) {
+        const int32_t h = (int32_t)(u % kQuadGroup);
+        const int64_t t = u / kQuadGroup;
+        const int32_t s = (int32_t)(t % p.nseg);
+        const int64_t g = t / p.nseg;
+        const int64_t q = ((g % ngroup) * kQuadGroup + h) * 4 + j;
+        const int64_t pl = g / ngroup;   // layer * 2 + plane
+        if (q >= p.num_jobs) continue;
+        const v4i jb = ((const_job_ptr)p.jobs)[q];
+        if (!job_ok(p, jb)) continue;
+        const int32_t blk = ((const_i32_ptr)p.bt)[(int64_t)jb.y * p.bt_stride + (int64_t)jb.z * p.nseg + s];
+        if (!blk_ok(p, blk)) continue;
+        const int32_t kv = (int32_t)(pl & 1);
+        const int32_t l = (int32_t)(pl >> 1);
+        const v4u *src = reinterpret_cast<const v4u *>(p.staging + (int64_t)jb.x * p.slot_bytes +
+                                                       (pl * p.nseg + s) * p.seg_bytes) + tid;
+        v4u *dst = reinterpret_cast<v4u *>(p.layers[l] + kv * p.kv_stride + (int64_t)blk * p.block_stride) + tid;
+        v4u a[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) a[r] = src[r * T];
+#pragma unroll
+        for (int r = 0; r < R; ++r) __builtin_nontemporal_store(a[r], dst + r * T);
+    }
+}
+
+// --------------------------------------------------------------------------
 // Group fast path (store, streaming retrieve): T lanes, R rows of T*16 bytes
 // per segment, SPW segments per workgroup (R * SPW = 16 vectors per lane).
 // --------------------------------------------------------------------------
@@ -375,6 +425,23 @@ bool launch_retrieve_pair(const CopyParams &p, hipStream_t s) {
     return true;
 }
 
+template <int R>
+void launch_retrieve_quad_r(const CopyParams &p, hipStream_t s) {
+    const int64_t units = ((int64_t)p.num_jobs + 4 * kQuadGroup - 1) / (4 * kQuadGroup) * kQuadGroup * p.nseg * p.L * 2;
+    hipLaunchKernelGGL(retrieve_quad_kernel<R>, dim3(grid_of(units)), dim3(1024), 0, s, p);
+}
+
+bool launch_retrieve_quad(const CopyParams &p, hipStream_t s) {
+    switch (rows_of(p.seg_bytes, 256 * 16)) {
+    case 1: launch_retrieve_quad_r<1>(p, s); return true;
+    case 2: launch_retrieve_quad_r<2>(p, s); return true;
+    case 4: launch_retrieve_quad_r<4>(p, s); return true;
+    case 8: launch_retrieve_quad_r<8>(p, s); return true;
+    case 16: launch_retrieve_quad_r<16>(p, s); return true;
+    default: return false;
+    }
+}
+
 bool launch_retrieve_fast(const CopyParams &p, hipStream_t s) {
     switch (rows_of(p.seg_bytes, 256 * 16)) {
     case 1: launch_retrieve_unit<1>(p, s); return true;
@@ -412,6 +479,7 @@ hipError_t launch_copy(const CopyParams &p, CopyKind kind, hipStream_t stream) {
     const bool retrieve = kind != kStore;
     const bool fast = kind == kRetrieve         ? launch_retrieve_fast(p, stream)
                       : kind == kRetrievePair   ? launch_retrieve_pair(p, stream) || launch_retrieve_fast(p, stream)
+                      : kind == kRetrieveQuad   ? launch_retrieve_quad(p, stream)
                       : kind == kRetrieveStream ? launch_group_fast<true>(p, stream)
                                                 : launch_group_fast<false>(p, stream);
     if (!fast) {

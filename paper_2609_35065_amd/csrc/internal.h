@@ -53,8 +53,9 @@ struct CopyParams {
 // units through the caches; kRetrievePair walks pairs of jobs and reads a
 // unit once for two jobs that share it; kRetrieveStream streams the staged
 // units with non-temporal loads in the store's workgroup shape, for job lists
-// that read each chunk once.
-enum CopyKind { kRetrieve, kRetrievePair, kRetrieveStream, kStore };
+// that read each chunk once; kRetrieveQuad copies one segment of four
+// consecutive jobs per 1024-lane workgroup.
+enum CopyKind { kRetrieve, kRetrievePair, kRetrieveStream, kRetrieveQuad, kStore };
 
 // Launchers (copy.hip, hash.hip).  Return hipSuccess or the launch error.
 hipError_t launch_copy(const CopyParams &p, CopyKind kind, hipStream_t stream);

@@ -32,7 +32,8 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (KV_COMMIT, KV_ENOSPC, KvIndex, KvLayout, KvPipeline, kv_build_jobs, kv_commit_should_stage_n,
+from . import (KV_COMMIT, KV_ENOSPC, KV_RETRIEVE_QUAD, KV_RETRIEVE_STREAM, RETRIEVE_KIND_NAMES, KvIndex, KvLayout,
+               KvPipeline, kv_build_jobs, kv_commit_should_stage_n,
                kv_group_jobs_by_slot, kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_pipelined,
                kv_retrieve_plan, kv_retrieve_scatter_as, kv_stage_out, kv_store_gather, make_layout)
 
@@ -106,6 +107,9 @@ class StagingPath:
         self.last_retrieve = np.zeros((0, 4), np.int32)
         self.last_store = np.zeros((0, 4), np.int32)
         self.retrieve_kind: Optional[int] = None
+        # planned retrieve variant -> variant to run instead (set by tune_retrieve)
+        self.retrieve_choice: Dict[int, int] = {}
+        self._last_nres = 0
 
     def set_batch(self, w) -> None:
         """Load a new request batch (tokens, offsets, block tables) that uses
@@ -293,7 +297,9 @@ class StagingPath:
             self._uploaded[par].record(self.stream)
             e = self._ev(timers, "retrieve")
             # the copy variant suited to how these jobs share staged chunks
-            self.retrieve_kind = kv_retrieve_plan(self.layout, self.h_retr.numpy()[:nres])
+            planned = kv_retrieve_plan(self.layout, self.h_retr.numpy()[:nres])
+            self.retrieve_kind = self.retrieve_choice.get(planned, planned)
+            self._last_nres = nres
             kv_retrieve_scatter_as(self.retrieve_kind, self.layout, self.staging_ptr, self.layers, self.bt,
                                    w.bt_stride, R, self.d_retr, nres, self.stream)
             if nres < nr:
@@ -327,6 +333,40 @@ class StagingPath:
         if evict_stored and ns:
             self.evict_last()
         return st
+
+    def tune_retrieve(self, reps: int = 5) -> Dict[str, float]:
+        """Choose, for this path's paged pool, between the planned retrieve and
+        the four-job-window retrieve (KV_RETRIEVE_QUAD) by timing both on the
+        resident jobs of the last pass: the faster (median of ``reps``
+        interleaved launches) is used for that plan from then on.  The
+        retrieve is idempotent, so the extra launches leave the pool as the
+        pass left it.  Returns the median times in ms by variant name; empty
+        when the last pass had no resident retrieve jobs or the plan was the
+        streaming retrieve (no staged chunk read twice)."""
+        self.stream.synchronize()
+        self.lookup_stream.synchronize()
+        n = self._last_nres
+        if n == 0:
+            return {}
+        w = self.batch
+        jobs = self.h_retr.numpy()[:n]
+        planned = kv_retrieve_plan(self.layout, jobs)
+        if planned == KV_RETRIEVE_STREAM:
+            return {}
+        kinds = [planned, KV_RETRIEVE_QUAD]
+        ms: Dict[int, List[float]] = {k: [] for k in kinds}
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for _ in range(reps):
+            for k in kinds:
+                a.record(self.stream)
+                kv_retrieve_scatter_as(k, self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride,
+                                       w.num_reqs, self.d_retr, n, self.stream)
+                b.record(self.stream)
+                b.synchronize()
+                ms[k].append(a.elapsed_time(b))
+        med = {k: float(np.median(v)) for k, v in ms.items()}
+        self.retrieve_choice[planned] = min(kinds, key=lambda k: med[k])
+        return {RETRIEVE_KIND_NAMES[k]: round(v, 4) for k, v in med.items()}
 
     def _ev(self, timers, name, stream=None):
         if timers is None:

@@ -154,7 +154,8 @@ def test_copy_calls_reject_bad_layouts_before_any_launch(over, code):
     lo = _layout(**over)
     L = kv.lib()
     layers = (ct.c_void_p * 128)(*([0x10000] * 128))
-    for f in (L.kv_retrieve_scatter, _as(L, kv.KV_RETRIEVE_PAIR), _as(L, kv.KV_RETRIEVE_STREAM), L.kv_store_gather):
+    for f in (L.kv_retrieve_scatter, _as(L, kv.KV_RETRIEVE_PAIR), _as(L, kv.KV_RETRIEVE_STREAM),
+              _as(L, kv.KV_RETRIEVE_QUAD), L.kv_store_gather):
         assert f(ct.byref(lo), 0x10000, layers, 0x10000, 10, 2, 0x10000, 1, None) == code
 
 
@@ -163,7 +164,7 @@ def test_copy_calls_reject_bad_pointers_before_any_launch():
     L = kv.lib()
     good = (ct.c_void_p * 2)(0x10000, 0x20000)
     for f in (L.kv_retrieve_scatter, _as(L, kv.KV_RETRIEVE_UNIT), _as(L, kv.KV_RETRIEVE_PAIR),
-              _as(L, kv.KV_RETRIEVE_STREAM), L.kv_store_gather):
+              _as(L, kv.KV_RETRIEVE_STREAM), _as(L, kv.KV_RETRIEVE_QUAD), L.kv_store_gather):
         assert f(ct.byref(lo), None, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EINVAL
         assert f(ct.byref(lo), 0x10008, good, 0x10000, 10, 2, 0x10000, 1, None) == kv.KV_EALIGN
         assert f(ct.byref(lo), 0x10000, (ct.c_void_p * 2)(0x10000, 0x20004), 0x10000, 10, 2, 0x10000, 1,
@@ -273,6 +274,6 @@ def test_retrieve_as_rejects_unknown_kinds():
     lo = _layout()
     L = kv.lib()
     layers = (ct.c_void_p * 2)(0x10000, 0x20000)
-    for kind in (-1, 3, 99):
+    for kind in (-1, 4, 99):
         assert L.kv_retrieve_scatter_as(kind, ct.byref(lo), 0x10000, layers, 0x10000, 10, 2, 0x10000, 1,
                                         None) == kv.KV_EINVAL

@@ -14,6 +14,7 @@ import pytest
 import torch
 
 import oracle
+import paper_2609_35065_amd as kv
 import workloads as W
 from oracle.pipeline import OraclePath
 from paper_2609_35065_amd.pipeline import StagingPath
@@ -30,11 +31,13 @@ def _seg_view(w, layer_tensor, kv, blk):
     return layer_tensor[off:off + seg], off
 
 
-def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy"):
+def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy", force_kind=None):
     w = W.make(name)
     print(f"[fullsize] {name}: {w.num_reqs} reqs, pool {w.pool_bytes() / 2**30:.1f} GiB, "
-          f"staging {w.staged_bytes() / 2**30:.1f} GiB, lower tier {lower_tier}", flush=True)
+          f"staging {w.staged_bytes() / 2**30:.1f} GiB, lower tier {lower_tier}, retrieve {force_kind}", flush=True)
     g = StagingPath(w, lower_tier=lower_tier)
+    if force_kind is not None:
+        g.retrieve_choice = {k: force_kind for k in (kv.KV_RETRIEVE_UNIT, kv.KV_RETRIEVE_PAIR, kv.KV_RETRIEVE_STREAM)}
     g.fill(STG_TAG, POOL_TAG, w.seed)
     g.prestage()
     o = OraclePath(w, with_kv=False)
@@ -42,6 +45,8 @@ def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy"):
     sg = g.run_pass(validate=True)
     so = o.run_pass()
     torch.cuda.synchronize()
+    if force_kind is not None:
+        assert g.retrieve_kind == force_kind
     nblk, nch, R = int(g.blk_off_h[-1]), int(g.chunk_off_h[-1]), w.num_reqs
     assert np.array_equal(g.h_block_hash.numpy()[:nblk].view(np.uint64), so["block_hash"])
     assert np.array_equal(g.h_chunk_slot.numpy()[:nch], so["chunk_slot"])
@@ -128,3 +133,10 @@ def test_full_size_sampled_pipelined_from_host(name):
     # batch by batch, before each batch's scatter
     sg, _ = check_full_size(name, lower_tier="pipelined")
     assert sg.staged_bytes > 0
+
+
+@pytest.mark.parametrize("name", ["l32-64x4096", "l48-64x4096", "l32-lognormal-p75", "l32-1024x1024-cap25-hbm",
+                                  "l32-64x4096-pad4096"])
+def test_full_size_sampled_quad_retrieve(name):
+    # the four-job-window retrieve, which tune_retrieve may choose for a pool
+    check_full_size(name, force_kind=kv.KV_RETRIEVE_QUAD)

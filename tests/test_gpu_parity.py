@@ -350,9 +350,9 @@ def test_out_of_range_jobs_are_skipped_on_device():
     oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs)
     kv.kv_store_gather(g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs, d_jobs, len(jobs))
     oracle.store_gather(o.layout, o.staging, o.layers, bt, jobs)
-    for kind in (kv.KV_RETRIEVE_PAIR, kv.KV_RETRIEVE_STREAM):
+    for kind in (kv.KV_RETRIEVE_PAIR, kv.KV_RETRIEVE_STREAM, kv.KV_RETRIEVE_QUAD):
         jobs2 = jobs.copy()
-        jobs2[-1, 0] = 2 + kind
+        jobs2[-1, 0] = (2 + kind) % w.num_slots
         kv.kv_retrieve_scatter_as(kind, g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs,
                                   torch.from_numpy(jobs2).cuda(), len(jobs2))
         oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs2)
@@ -364,8 +364,8 @@ def test_out_of_range_jobs_are_skipped_on_device():
 
 @pytest.mark.parametrize("layout,pad", [("kv_first", 0), ("block_first", 48)])
 @pytest.mark.parametrize("si", range(len(SHAPES)))
-@pytest.mark.parametrize("sharing", ["distinct", "pairs", "mixed"])
-@pytest.mark.parametrize("kind", [1, 2])
+@pytest.mark.parametrize("sharing", ["distinct", "pairs", "groups", "mixed"])
+@pytest.mark.parametrize("kind", [1, 2, 3])
 def test_retrieve_variants_match_oracle(kind, sharing, si, layout, pad):
     # Every variant must give the oracle's bytes for any job list: distinct slots, slots shared by aligned
     # pairs, and a mixed list (odd length, pairs that straddle two slots, out-of-range jobs in between).
@@ -379,6 +379,8 @@ def test_retrieve_variants_match_oracle(kind, sharing, si, layout, pad):
         jobs[:, 0] = np.arange(n) % w.num_slots
     elif sharing == "pairs":
         jobs[:, 0] = (np.arange(n) // 2) % w.num_slots
+    elif sharing == "groups":
+        jobs[:, 0] = (np.arange(n) // 8) % w.num_slots
     else:
         jobs[:, 0] = (np.arange(n) // 3) % w.num_slots
         jobs = np.concatenate([jobs[: n - 1 + (n % 2)], [[w.num_slots, 0, 0, 0], [0, w.num_reqs, 0, 0]]])
@@ -441,6 +443,39 @@ def test_overlapped_passes_match_sequential_oracle(evict):
         assert sg.dropped == so["dropped"]
         if i + 1 < n:
             g.launch_lookup()
+    torch.cuda.synchronize()
+    assert np.array_equal(g.staging_view().cpu().numpy(), o.staging)
+    for l in range(len(g.layers)):
+        assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
+    _free(g, o)
+
+
+@pytest.mark.parametrize("workload_seed", [78, 79])
+def test_tuned_retrieve_passes_match_oracle(workload_seed):
+    # tune_retrieve times the planned retrieve against the four-job-window one on the live pool (re-running
+    # the last pass's retrieve, which is idempotent) and keeps the faster; later passes must still give the
+    # oracle's bytes, whichever was chosen.
+    shape = W.KVShape(2, 2, 64, 2, 16, 64)
+    w = W.small_random(workload_seed, shape, num_reqs=12, max_len=6 * 64 + 5)
+    g = StagingPath(w)
+    g.fill(STG_TAG, POOL_TAG, w.seed, True)
+    g.prestage()
+    o = OraclePath(w, kv_seed=w.seed, finite=True, staging_tag=STG_TAG, pool_tag_base=POOL_TAG)
+    o.prestage()
+    g.run_pass(evict_stored=False)
+    o.run_pass(evict_stored=False)
+    tuned = g.tune_retrieve(reps=3)
+    if len(g.last_retrieve):
+        assert "quad" in tuned and len(tuned) == 2 and all(v > 0 for v in tuned.values())
+        assert set(g.retrieve_choice.values()) <= {kv.KV_RETRIEVE_QUAD, kv.KV_RETRIEVE_UNIT, kv.KV_RETRIEVE_PAIR}
+    torch.cuda.synchronize()
+    assert np.array_equal(g.staging_view().cpu().numpy(), o.staging)
+    for l in range(len(g.layers)):
+        assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
+    for i in range(3):
+        g.run_pass(evict_stored=True)
+        so = o.run_pass(evict_stored=True)
+        assert np.array_equal(g.last_retrieve, so["retrieve"]), i
     torch.cuda.synchronize()
     assert np.array_equal(g.staging_view().cpu().numpy(), o.staging)
     for l in range(len(g.layers)):
