@@ -341,12 +341,14 @@ class StagingPath:
         interleaved launches) is used for that plan from then on.  The
         retrieve is idempotent, so the extra launches leave the pool as the
         pass left it.  Returns the median times in ms by variant name; empty
-        when the last pass had no resident retrieve jobs or the plan was the
-        streaming retrieve (no staged chunk read twice)."""
+        when the last pass had no resident retrieve jobs, the plan was the
+        streaming retrieve (no staged chunk read twice), or the staged chunks
+        are read from host memory in place (zero-copy: every window quarter
+        would read its segment over the host link, 5-7x slower)."""
         self.stream.synchronize()
         self.lookup_stream.synchronize()
         n = self._last_nres
-        if n == 0:
+        if n == 0 or (self.staging_host is not None and not self.staged_mode):
             return {}
         w = self.batch
         jobs = self.h_retr.numpy()[:n]
