@@ -3,8 +3,9 @@
 A pass is:  hash (kv_hash_prefix) -> lookup (kv_lookup) -> one device-to-host
 copy of the lookup result -> host job build (kv_build_jobs) and commitment
 decisions (kv_commit_should_stage_n) -> one host-to-device copy of the jobs ->
-retrieve scatter (kv_retrieve_plan picks the copy variant, kv_retrieve_scatter_as
-runs it) -> store gather (kv_store_gather) ->
+retrieve scatter (kv_retrieve_plan picks the copy variant, or the variant
+tune_retrieve found faster for that plan on this path's pool;
+kv_retrieve_scatter_as runs it) -> store gather (kv_store_gather) ->
 index update (kv_index_insert; optionally kv_index_erase of what was just
 stored, which returns the batch to its starting state so that passes can be
 repeated).
