@@ -119,6 +119,40 @@ def _cpu_model() -> str:
     return "unknown"
 
 
+def _retrieve_write_bound(path, torch, reps: int = 5):
+    """The timed retrieve's writes on their own: the same jobs, variant and
+    destination blocks, but every job reading one staged chunk (which stays in
+    L2), so HBM sees only the scattered 32 KiB writes.  Its time bounds the
+    retrieve on this pool from below; it runs after the timed steps and
+    leaves the written blocks holding that chunk."""
+    import numpy as np
+    import paper_2609_35065_amd as kv
+    n = path._last_nres
+    # (the streaming retrieve's non-temporal loads would not keep the one chunk in L2)
+    if n == 0 or path.staging_host is not None or path.retrieve_kind not in (
+            kv.KV_RETRIEVE_UNIT, kv.KV_RETRIEVE_PAIR, kv.KV_RETRIEVE_QUAD):
+        return None
+    w = path.batch
+    jobs = path.h_retr.numpy()[:n].copy()
+    jobs[:, 0] = jobs[0, 0]
+    d_jobs = torch.from_numpy(jobs).to(path.dev)
+    s = path.stream
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ms = []
+    for _ in range(reps):
+        a.record(s)
+        kv.kv_retrieve_scatter_as(path.retrieve_kind, path.layout, path.staging_ptr, path.layers, path.bt,
+                                  w.bt_stride, w.num_reqs, d_jobs, n, s)
+        b.record(s)
+        b.synchronize()
+        ms.append(a.elapsed_time(b))
+    t = float(np.median(ms))
+    written = n * w.shape.slot_bytes
+    return {"ms": round(t, 4), "GB/s_written": round(written / (t * 1e-3) / 1e9, 1),
+            "what": "the timed retrieve's jobs and variant with every job reading one staged chunk: its "
+                    "scattered writes alone (median of 5)"}
+
+
 def _calibration_copy(torch, reps: int = 5) -> dict:
     """A plain contiguous copy of known size, run by the library's own copy
     kernel: one layer, block size == chunk size, block_first paged layout and
@@ -464,12 +498,15 @@ def main() -> int:
                 lt["stage_ms"] = round(k_ms["stage"], 4)
                 lt["stage_GB/s"] = round(stats.staged_bytes / (k_ms["stage"] * 1e-3) / 1e9, 1)
         line["config"]["lower_tier"] = lt
+    wb = _retrieve_write_bound(path, torch) if not args.no_fill else None
     del path
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     if not args.no_fill:
         line["practical_peak"] = {"torch_device_copy_GB/s": round(_device_copy_gbs(torch), 1),
                                   "library_contiguous_copy_GB/s": _calibration_copy(torch)["GB/s_rw"]}
+        if wb:
+            line["practical_peak"]["retrieve_writes_only"] = wb
         if w.staging_in_host:
             line["practical_peak"].update(_host_link_gbs(torch))
         props = torch.cuda.get_device_properties(0)
