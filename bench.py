@@ -506,6 +506,9 @@ def main() -> int:
         line["practical_peak"] = {"torch_device_copy_GB/s": round(_device_copy_gbs(torch), 1),
                                   "library_contiguous_copy_GB/s": _calibration_copy(torch)["GB/s_rw"]}
         if wb:
+            # the retrieve's algorithmic bytes moved at the pool's own scattered-write rate
+            wb["alg_bytes_at_this_rate_ms"] = round(r_alg / (wb["GB/s_written"] * 1e9) * 1e3, 4)
+            wb["retrieve_frac_of_this_rate"] = round(wb["alg_bytes_at_this_rate_ms"] / k_ms["retrieve"], 4)
             line["practical_peak"]["retrieve_writes_only"] = wb
         if w.staging_in_host:
             line["practical_peak"].update(_host_link_gbs(torch))
