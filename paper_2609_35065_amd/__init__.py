@@ -32,10 +32,10 @@ HASH_BLOCK_TOKENS = 16
 # every symbol include/tempokv.h declares
 EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
            "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
-           "kv_store_gather", "kv_group_jobs_by_slot", "kv_validate_jobs", "kv_commit_should_stage", "kv_strerror",
-           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out", "kv_pipeline_create", "kv_commit_should_stage_n", "kv_retrieve_plan",
-           "kv_retrieve_scatter_as",
-           "kv_pipeline_destroy", "kv_retrieve_pipelined"]
+           "kv_retrieve_plan", "kv_retrieve_scatter_as", "kv_store_gather", "kv_group_jobs_by_slot",
+           "kv_validate_jobs", "kv_commit_should_stage", "kv_commit_should_stage_n", "kv_strerror",
+           "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out",
+           "kv_pipeline_create", "kv_pipeline_destroy", "kv_retrieve_pipelined"]
 
 
 class KvError(RuntimeError):
