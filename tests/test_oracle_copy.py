@@ -185,10 +185,14 @@ def test_out_of_range_jobs_and_blocks_touch_nothing():
         assert set(changed) <= {int(bt[0, 0]), int(bt[0, 3])}
 
 
-def test_one_by_one_sources_agree_with_full_copies():
+@pytest.mark.parametrize("repeat", [False, True])
+def test_one_by_one_sources_agree_with_full_copies(repeat):
+    # repeat: a later job names the destination of an earlier one (the same blocks for the scatter, the same
+    # slot for the gather); in the full copies the later job's bytes land last, and the one-by-one forms must
+    # name the later job too
     shape, lo, bt, staging, layers, nb = _setup(41, 2, 2, 64, 2, 16, 64, "block_first")
     nseg = shape.blocks_per_chunk
-    jobs = np.array([[3, 0, 2, 0], [1, 1, 0, 0], [3, 2, 1, 0]], np.int32)
+    jobs = np.array([[3, 0, 2, 0], [1, 1, 0, 0], [3, 2, 1, 0]] + ([[4, 1, 0, 0]] if repeat else []), np.int32)
     out = [np.zeros_like(a) for a in layers]
     oracle.retrieve_scatter(lo, staging, out, bt, jobs)
     seg = shape.seg_bytes
@@ -201,7 +205,7 @@ def test_one_by_one_sources_agree_with_full_copies():
                     assert np.all(pv[kv, blk] == 0)
                 else:
                     assert np.array_equal(pv[kv, blk], staging[src:src + seg])
-    sj = np.array([[5, 2, 2, 0], [0, 0, 1, 0]], np.int32)
+    sj = np.array([[5, 2, 2, 0], [0, 0, 1, 0]] + ([[5, 1, 1, 0]] if repeat else []), np.int32)
     st = np.zeros_like(staging)
     oracle.store_gather(lo, st, layers, bt, sj)
     for slot in range(6):

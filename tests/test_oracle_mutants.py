@@ -1,0 +1,136 @@
+"""The pins must catch plausible mistakes in the oracle.
+
+Each case plants one mistake in a copy of ``oracle/tempokv_oracle.c`` (a
+wrong shift or constant, a dropped term, a swapped or off-by-one index, a
+boundary moved by one, a rule inverted), compiles it, and runs the pin tests
+of the function it touches against it in a child process.  The case passes
+only if some pin fails.  The frozen golden hash vectors are left out of those
+runs: they were written by the oracle itself and only guard against
+regressions, so they must not be what catches a mistake.
+
+Changes to parts of the hash that are this library's own choice (the exact
+position word, the chain constant) are not mistakes with respect to any pin:
+the paper does not define the hash.  They are listed as such and checked to
+change the function, which the GPU parity tests then hold the kernel to."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "tempokv_oracle.c")
+
+HASH = ["tests/test_oracle_hash.py", "tests/test_oracle_properties.py"]
+LOOKUP = ["tests/test_oracle_lookup.py"]
+COPY = ["tests/test_oracle_copy.py", "tests/test_oracle_properties.py"]
+COMMIT = ["tests/test_oracle_commit.py", "tests/test_oracle_properties.py"]
+
+# (name, pin tests, text in the oracle, planted replacement)
+MUTANTS = [
+    ("mix_shift_30", HASH, "z = (z ^ (z >> 30))", "z = (z ^ (z >> 29))"),
+    ("mix_multiplier", HASH, "0xBF58476D1CE4E5B9ull", "0xBF58476D1CE4E5BBull"),
+    ("mix_final_shift", HASH, "return z ^ (z >> 31);", "return z ^ (z >> 32);"),
+    ("digest_xor_not_sum", HASH, "d += or_mix64(word);", "d ^= or_mix64(word);"),
+    ("digest_drops_position", HASH, "+ ((uint64_t)(j + 1) << 32)", "+ ((uint64_t)1 << 32)"),
+    ("chain_not_chained", HASH, "h = or_mix64(h ^ d ^ OR_GAMMA);", "h = or_mix64(seed ^ d ^ OR_GAMMA);"),
+    ("chain_seed_ignored", HASH, "uint64_t h = seed;", "uint64_t h = 0;"),
+    ("chain_block_off_by_one", HASH, "tokens + tok_off[r] + b * OR_HASH_BLOCK", "tokens + tok_off[r] + b * OR_HASH_BLOCK + 1"),
+    ("lookup_not_prefix", LOOKUP, "if (s < 0) still_prefix = 0;", ""),
+    ("lookup_first_block_key", LOOKUP, "uint64_t key = block_hash[blk_off[r] + (j + 1) * blocks_per_chunk - 1];\n"
+     "            int32_t s = or_index_find", "uint64_t key = block_hash[blk_off[r] + j * blocks_per_chunk];\n"
+     "            int32_t s = or_index_find"),
+    ("jobs_retrieve_one_too_many", LOOKUP, "if (j < hit_chunks[r]) {", "if (j <= hit_chunks[r]) {"),
+    ("jobs_store_indexed_chunks", LOOKUP, "if (s >= 0) continue;", "if (s >= 0 && 0) continue;"),
+    ("jobs_no_dedup", LOOKUP, "if (seen) continue;", "if (seen && 0) continue;"),
+    ("jobs_slots_reversed", LOOKUP, "store[ns].slot = free_slots[ns];", "store[ns].slot = free_slots[num_free - 1 - ns];"),
+    ("jobs_dropped_not_counted", LOOKUP, "if (ns >= num_free) { nd++; continue; }", "if (ns >= num_free) { continue; }"),
+    ("scatter_layer_plane_swapped", COPY, "int64_t src = jb->slot * slot_bytes\n"
+     "                                    + ((((int64_t)l * 2 + kv)", "int64_t src = jb->slot * slot_bytes\n"
+     "                                    + ((((int64_t)kv * lo->L + l)"),
+    ("scatter_token_dropped", COPY, "int64_t dst = kv * lo->kv_stride + blk * lo->block_stride\n"
+     "                                    + ((int64_t)t * HD + x)", "int64_t dst = kv * lo->kv_stride + blk * lo->block_stride\n"
+     "                                    + ((int64_t)0 * HD + x)"),
+    ("scatter_block_bound", COPY, "if (blk < 0 || blk >= lo->num_blocks) continue;\n                    for (int32_t t = 0; t < lo->B; t++)\n"
+     "                        for (int64_t x = 0; x < HD; x++)\n                            for (int32_t c = 0; c < lo->e; c++) {\n"
+     "                                int64_t src = jb->slot", "if (blk < 0 || blk > lo->num_blocks) continue;\n                    for (int32_t t = 0; t < lo->B; t++)\n"
+     "                        for (int64_t x = 0; x < HD; x++)\n                            for (int32_t c = 0; c < lo->e; c++) {\n"
+     "                                int64_t src = jb->slot"),
+    ("job_chunk_bound", COPY, "(int64_t)(jb->chunk + 1) * nseg > bt_stride", "(int64_t)jb->chunk * nseg > bt_stride"),
+    ("gather_kv_stride_dropped", COPY, "int64_t src = kv * lo->kv_stride + blk * lo->block_stride", "int64_t src = blk * lo->block_stride"),
+    ("gather_segment_off_by_one", COPY, "+ ((((int64_t)l * 2 + kv) * lo->C + (int64_t)i * lo->B + t) * HD + x) * lo->e + c;\n"
+     "                                int64_t src", "+ ((((int64_t)l * 2 + kv) * lo->C + (int64_t)(i + 1) % nseg * lo->B + t) * HD + x) * lo->e + c;\n"
+     "                                int64_t src"),
+    ("scatter_source_segment", COPY, "(((int64_t)layer * 2 + kv) * lo->C + (int64_t)i * lo->B) * HD * lo->e",
+     "(((int64_t)layer * 2 + kv) * lo->C + (int64_t)i) * HD * lo->e"),
+    ("gather_source_first_not_last", COPY, "*blk_out = blk;\n        found = 1;", "if (!found) *blk_out = blk;\n        found = 1;"),
+    ("commit_strict_laxity", COMMIT, "int eligible = (ttu <= ttr)", "int eligible = (ttu < ttr)"),
+    ("commit_no_budget_check", COMMIT, "(claim_total_bytes <= budget_bytes) && ", ""),
+    ("commit_new_vs_total", COMMIT, "(claim_new_bytes <= free_protected_bytes)", "(claim_total_bytes <= free_protected_bytes)"),
+    ("commit_outcomes_swapped", COMMIT, "return retrieval_requested ? OR_ORDINARY : OR_BLOCKED;",
+     "return retrieval_requested ? OR_BLOCKED : OR_ORDINARY;"),
+    ("commit_request_not_eligible", COMMIT, "|| (retrieval_requested != 0)", ""),
+]
+
+# the library's own choices inside the hash: no pin can tell them from the planted variant
+DEFINITIONAL = [
+    ("position_word_offset", "((uint64_t)(j + 1) << 32)", "((uint64_t)(j + 2) << 32)"),
+    ("chain_constant", "h = or_mix64(h ^ d ^ OR_GAMMA);", "h = or_mix64(h ^ d);"),
+    # sign-extending ids is another injective encoding of (position, id); it differs only for negative ids
+    ("signed_token_words", "(uint64_t)(uint32_t)tok16[j]", "(uint64_t)(int64_t)tok16[j]"),
+]
+
+
+def _compile(src_text: str, out: str) -> None:
+    c = out[:-3] + ".c"
+    with open(c, "w") as f:
+        f.write(src_text)
+    subprocess.check_call(["gcc", "-O1", "-std=c11", "-fPIC", "-shared", "-w", "-o", out, c, "-lm"])
+
+
+def _run_pins(lib_path: str, tests) -> subprocess.CompletedProcess:
+    env = dict(os.environ, TEMPOKV_ORACLE_LIB=lib_path, HYPOTHESIS_PROFILE="default")
+    return subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", "-k", "not golden",
+                           *tests], cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
+
+
+def test_unplanted_copy_passes_the_pins(tmp_path):
+    # the harness itself: the oracle as committed, built the same way, passes every pin
+    so = str(tmp_path / "liboracle_ref.so")
+    _compile(open(SRC).read(), so)
+    r = _run_pins(so, sorted(set(HASH + LOOKUP + COPY + COMMIT)))
+    assert r.returncode == 0, r.stdout[-3000:]
+
+
+@pytest.mark.parametrize("name,tests,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(tmp_path, name, tests, old, new):
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"{name}: the text to change must occur exactly once"
+    so = str(tmp_path / f"liboracle_{name}.so")
+    _compile(src.replace(old, new), so)
+    r = _run_pins(so, tests)
+    # exit 1: a pin failed; a negative code: the planted mistake crashed a pin run
+    assert r.returncode == 1 or r.returncode < 0, f"{name} survived the pins:\n{r.stdout[-2000:]}"
+
+
+@pytest.mark.parametrize("name,old,new", DEFINITIONAL, ids=[m[0] for m in DEFINITIONAL])
+def test_definitional_changes_change_the_hash(tmp_path, name, old, new):
+    import ctypes as ct
+    src = open(SRC).read()
+    assert src.count(old) == 1
+    outs = []
+    for i, text in enumerate((src, src.replace(old, new))):
+        so = str(tmp_path / f"liboracle_{name}_{i}.so")
+        _compile(text, so)
+        L = ct.CDLL(so)
+        L.or_hash_prefix.restype = ct.c_int
+        toks = np.arange(-32, 32, dtype=np.int32) * 1000003
+        off = np.array([0, 64], np.int64)
+        boff = np.array([0, 4], np.int64)
+        out = np.zeros(4, np.uint64)
+        P = lambda a, t: a.ctypes.data_as(ct.POINTER(t))
+        assert L.or_hash_prefix(P(toks, ct.c_int32), P(off, ct.c_int64), 1, ct.c_uint64(7), P(boff, ct.c_int64),
+                                P(out, ct.c_uint64)) == 0
+        outs.append(out.copy())
+    assert np.all(outs[0] != outs[1])
