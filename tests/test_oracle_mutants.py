@@ -134,3 +134,75 @@ def test_definitional_changes_change_the_hash(tmp_path, name, old, new):
                                 P(out, ct.c_uint64)) == 0
         outs.append(out.copy())
     assert np.all(outs[0] != outs[1])
+
+
+# ---------------------------------------------------------------------------
+# The controller oracle (plain Python): the same idea, the planted copy loaded
+# in place of oracle.controller in a child process that runs its pin tests.
+# ---------------------------------------------------------------------------
+CTRL_SRC = os.path.join(ROOT, "oracle", "controller.py")
+CTRL_PINS = ["tests/test_oracle_controller.py"]
+_RUNNER = (
+    "import sys, importlib.util\n"
+    "import oracle\n"
+    "spec = importlib.util.spec_from_file_location('oracle.controller', sys.argv[1])\n"
+    "m = importlib.util.module_from_spec(spec)\n"
+    "sys.modules['oracle.controller'] = m\n"
+    "spec.loader.exec_module(m)\n"
+    "oracle.controller = m\n"
+    "import pytest\n"
+    "sys.exit(pytest.main(['-x', '-q', '-p', 'no:cacheprovider', *sys.argv[2:]]))\n")
+
+# Not listed: evaluating waiting claims before requested ones.  In this model every event gets its own
+# control point and slots are filled greedily, so a claim becomes requested only at a control point where no
+# other claim's eligibility or fit changed: the two orders decide the same, and no pin can tell them apart.
+CTRL_MUTANTS = [
+    ("shared_counted_twice", "            if prot[o] == 0:\n                P += obj_bytes[o]",
+     "            if True:\n                P += obj_bytes[o]"),
+    ("release_keeps_reservation", "                    if prot[o] == 0:\n                        P -= obj_bytes[o]",
+     "                    if prot[o] == 0 and False:\n                        P -= obj_bytes[o]"),
+    ("stage_reads_not_coalesced", "if not resident[o] and not queued[o]:\n                start", "if not resident[o]:\n                start"),
+    ("state_ttr_ignores_queue", "        tail = max(busy_until, now)", "        tail = now"),
+    ("state_ttr_first_object_decides", "                tail = tail + obj_bytes[o] / cfg.stage_rate\n                t_end = max(t_end, tail)",
+     "                tail = tail + obj_bytes[o] / cfg.stage_rate\n                t_end = tail if t_end == now else t_end"),
+    ("tempo_uses_static_ttr", "            ttu, ttr = (ttu_map[i] if i in ttu_map else math.inf), ttr_state(i)",
+     "            ttu, ttr = (ttu_map[i] if i in ttu_map else math.inf), ttr_static(i)"),
+    ("ttu_ignores_busy_slots", "        slots = [projected_end(a) for a in active] + [now] * (cfg.max_active - len(active))",
+     "        slots = [now] * cfg.max_active"),
+    ("ttu_counts_own_service", "            out[w] = s0 - now", "            out[w] = s0 + svc[w] - now"),
+    ("queue_k_off_by_one", "(pos is not None and pos < cfg.queue_k)", "(pos is not None and pos <= cfg.queue_k)"),
+    ("transfer_before_stage_ready", "            if state[i] == STAGEREADY:\n                state[i] = TRANSFERRING",
+     "            if state[i] in (STAGEREADY, STAGING):\n                state[i] = TRANSFERRING"),
+    ("release_at_request_end", "        elif kind == EV_TRANSFER_END:\n            if state[a] == TRANSFERRING:",
+     "        elif kind == EV_TRANSFER_END:\n            if state[a] == TRANSFERRING and False:"),
+    ("cost_not_per_request", "C=area / GIB / N", "C=area / GIB"),
+    ("no_budget_headroom", "int(cfg.budget - P), int(new)", "int(cfg.budget), int(new)"),
+    ("new_bytes_count_protected", "        new = sum(obj_bytes[o] for o in uniq[i] if prot[o] == 0)",
+     "        new = sum(obj_bytes[o] for o in uniq[i])"),
+    ("no_ticks", "            push((a + 1) * cfg.tick, EV_TICK, a + 1)", "            pass"),
+    ("demand_commits_early", "            ttu, ttr = math.inf, 0.0\n        elif pol == IMMEDIATE:",
+     "            ttu, ttr = 0.0, 0.0\n        elif pol == IMMEDIATE:"),
+    ("ordinary_reads_free", "                fetch_end[i] = max(now, busy_until) + nonres / cfg.stage_rate",
+     "                fetch_end[i] = now"),
+    ("transfer_time_dropped", "                t_x = now + total[i] / cfg.gpu_rate\n                first_token[i]",
+     "                t_x = now\n                first_token[i]"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", CTRL_MUTANTS, ids=[m[0] for m in CTRL_MUTANTS])
+def test_controller_pins_catch_planted_mistake(tmp_path, name, old, new):
+    src = open(CTRL_SRC).read()
+    assert src.count(old) == 1, f"{name}: the text to change must occur exactly once"
+    path = tmp_path / "controller.py"
+    path.write_text(src.replace(old, new))
+    r = subprocess.run([sys.executable, "-c", _RUNNER, str(path), *CTRL_PINS], cwd=ROOT, capture_output=True,
+                       text=True, timeout=600)
+    assert r.returncode == 1 or r.returncode < 0, f"{name} survived the pins:\n{r.stdout[-2000:]}"
+
+
+def test_controller_unplanted_copy_passes_the_pins(tmp_path):
+    path = tmp_path / "controller.py"
+    path.write_text(open(CTRL_SRC).read())
+    r = subprocess.run([sys.executable, "-c", _RUNNER, str(path), *CTRL_PINS], cwd=ROOT, capture_output=True,
+                       text=True, timeout=600)
+    assert r.returncode == 0, r.stdout[-3000:]
