@@ -481,3 +481,32 @@ def test_tuned_retrieve_passes_match_oracle(workload_seed):
     for l in range(len(g.layers)):
         assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
     _free(g, o)
+
+
+@pytest.mark.parametrize("kind", ["store", 0, 1, 2, 3])
+def test_million_job_lists_match_oracle(kind):
+    # 2^20 jobs (grids of 2^20-2^22 workgroups) cycling over a few (slot, request, chunk) triples: every
+    # repeat of a triple copies the same bytes to the same place, so the result is the oracle's over the
+    # distinct triples, whatever order the repeats land in
+    shape = W.KVShape(1, 2, 64, 2, 16, 64)                  # 4 KiB segments, 4 per chunk
+    w = W.small_random(501, shape, num_reqs=6, max_len=4 * 64)
+    g, o = _pair(w)
+    base = W.random_retrieve_jobs(w, 501, slots_used=w.num_slots)[:5]
+    assert len(base) == 5 and w.num_slots >= 5
+    if kind == "store":
+        base[:, 0] = np.arange(len(base))                   # one slot per distinct triple
+    n = 1 << 20
+    jobs = np.ascontiguousarray(base[np.arange(n) % len(base)], np.int32)
+    d_jobs = torch.from_numpy(jobs).cuda()
+    print(f"[million] kind {kind}: {n} jobs over {len(base)} triples, shape {shape}", flush=True)
+    if kind == "store":
+        kv.kv_store_gather(g.layout, g.staging, g.layers, g.bt, w.bt_stride, w.num_reqs, d_jobs, n)
+        oracle.store_gather(o.layout, o.staging, o.layers, w.block_tables, base)
+    else:
+        kv.kv_retrieve_scatter_as(kind, g.layout, g.staging, g.layers, g.bt, w.bt_stride, w.num_reqs, d_jobs, n)
+        oracle.retrieve_scatter(o.layout, o.staging, o.layers, w.block_tables, base)
+    torch.cuda.synchronize()
+    assert np.array_equal(g.staging.cpu().numpy(), o.staging)
+    for l in range(len(g.layers)):
+        assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
+    _free(g, o)
