@@ -67,14 +67,14 @@ def _load_traffic(kernel: str, workload: str):
         return None
 
 
-def _cpu_baseline(shape_name: str):
+def _cpu_baseline(shape):
     """The CPU oracle on a bounded sample with the benchmark's KV shape:
     8 requests x 4096 tokens, 50% prefix from 2 shared prefixes (64 retrieve
-    and 64 store jobs per pass, 8 GiB moved), two passes (stored chunks are
-    evicted after each, as in the benchmark), single thread."""
+    and 64 store jobs per pass, 8 GiB moved per pass at 32 layers), two passes
+    (stored chunks are evicted after each, as in the benchmark), single
+    thread."""
     import workloads as W
     from oracle.pipeline import OraclePath
-    shape = W.SHAPE_32L if shape_name == "l32" else W.SHAPE_80L
     R, passes = 8, 2
     w = W._assemble("cpu-sample", shape, 2, [4096] * R, [r % 2 for r in range(R)], [2048] * R, 2,
                     prestage=[(p, j) for p in range(2) for j in range(8)], num_slots=16 + 8 * R, pool_factor=1.25)
@@ -517,7 +517,7 @@ def main() -> int:
                        "memory_GiB": round(props.total_memory / 2**30, 1), "clocks": _clocks()}
     if not args.no_cpu_baseline and not args.no_fill:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = _cpu_baseline("l80" if w.shape.num_layers == 80 else "l32")
+        line["cpu_baseline"] = _cpu_baseline(w.shape)
     print(json.dumps(line), flush=True)
     return 0
 
