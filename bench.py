@@ -487,6 +487,9 @@ def main() -> int:
                   "Mtok/s)",
         "source_digest": _src_digest(),
     }
+    if not w.staging_in_host:
+        # the same step in HBM terms: unique staged reads + writes of the retrieve, reads + writes of the store
+        line["step_hbm_GB/s"] = round((r_alg + s_bytes) / (ms_step * 1e-3) / 1e9, 1)
     for name, key in (("retrieve", "retrieve_scatter"), ("store", "store_gather"), ("hash", "hash_prefix"),
                       ("lookup", "lookup")):
         line["kernels"][key].update(spread(name))
