@@ -5,6 +5,7 @@ the oracle on the same seeded inputs, and compares outputs exactly: block
 hashes, lookup results, job lists, and every byte of the staging buffer and
 the paged pool.  Inputs come from the workload generator only."""
 import copy
+import os
 
 import numpy as np
 import pytest
@@ -510,3 +511,33 @@ def test_million_job_lists_match_oracle(kind):
     for l in range(len(g.layers)):
         assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
     _free(g, o)
+
+
+def test_many_random_shapes_every_variant():
+    # A wider sweep than the forty above: TEMPOKV_SOAK_SHAPES random shapes (300 by default; 3,000 have been
+    # run), each with two whole passes and then every retrieve variant on a random job list (grouped or not),
+    # every byte compared with the oracle.
+    n = int(os.environ.get("TEMPOKV_SOAK_SHAPES", "300"))
+    for k, shape in enumerate(W.random_shapes(3030, n)):
+        layout = ["kv_first", "block_first"][k % 2]
+        pad = [0, 16, 4096, 48, 32][k % 5]
+        w = W.small_random(5000 + k, shape, num_reqs=5 + k % 4, max_len=3 * shape.chunk_tokens + 7 * (k % 5),
+                           paged_layout=layout, block_pad=pad)
+        g, o = _pair(w)
+        for p in range(2):
+            sg, so = g.run_pass(validate=True), o.run_pass()
+            _compare_pass(g, o, sg, so)
+        jobs = W.random_retrieve_jobs(w, 5000 + k, slots_used=max(1, w.num_slots // 3))
+        if len(jobs):
+            jobs = np.ascontiguousarray(kv.kv_group_jobs_by_slot(jobs) if k % 2 else jobs, np.int32)
+            d_jobs = torch.from_numpy(jobs).cuda()
+            for kind in (kv.KV_RETRIEVE_UNIT, kv.KV_RETRIEVE_PAIR, kv.KV_RETRIEVE_STREAM, kv.KV_RETRIEVE_QUAD):
+                kv.kv_retrieve_scatter_as(kind, g.layout, g.staging, g.layers, g.bt, w.bt_stride, w.num_reqs,
+                                          d_jobs, len(jobs))
+            oracle.retrieve_scatter(o.layout, o.staging, o.layers, w.block_tables, jobs)
+            torch.cuda.synchronize()
+            for l in range(len(g.layers)):
+                assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l]), (k, shape, l)
+        _free(g, o)
+        if k % 100 == 99:
+            print(f"[shapes] {k + 1}/{n} ok", flush=True)
