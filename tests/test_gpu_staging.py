@@ -110,6 +110,50 @@ def test_retrieve_pipelined_matches_oracle(max_batches, spb, same_stream, groupe
         assert np.array_equal(d[s], h[s]) if s in named else np.all(d[s] == SENT_STG)
 
 
+def test_retrieve_pipelined_random_sweep():
+    # 60 random shapes and layouts, each with a random batch size (1-5 slots, or everything), pipeline size
+    # (2-64 events), one or two streams, grouped or ungrouped jobs: pool and staging bytes against the oracle
+    rng = np.random.default_rng(4242)
+    shapes = W.random_shapes(4242, 60)
+    for k, shape in enumerate(shapes):
+        w = W.small_random(900 + k, shape, num_reqs=4 + k % 4, max_len=4 * shape.chunk_tokens + 11,
+                           paged_layout=["kv_first", "block_first"][k % 2], block_pad=[0, 16, 48][k % 3])
+        kv_stride, block_stride = w.strides()
+        lo = kv.make_layout(shape.num_layers, shape.kv_heads, shape.head_dim, shape.elem_bytes, shape.block_size,
+                            shape.chunk_tokens, w.num_blocks, w.num_slots, kv_stride, block_stride)
+        olo = oracle.make_layout(shape, w.num_blocks, w.num_slots, kv_stride, block_stride)
+        sb, S = shape.slot_bytes, w.num_slots
+        jobs = W.random_retrieve_jobs(w, 900 + k, slots_used=max(1, int(rng.integers(1, S + 1))))
+        if len(jobs) == 0:
+            continue
+        if rng.integers(0, 2):
+            jobs = kv.kv_group_jobs_by_slot(jobs)
+        jobs = np.ascontiguousarray(jobs, np.int32)
+        spb = int(rng.choice([1, 2, 3, 5, 1000]))
+        max_batches = int(rng.choice([2, 3, 8, 64]))
+        host = _pinned_kv(S * sb, 1, 900 + k)
+        stg = torch.full((S * sb,), SENT_STG, dtype=torch.uint8, device="cuda")
+        layers = [torch.full((w.layer_bytes(),), SENT_POOL, dtype=torch.uint8, device="cuda")
+                  for _ in range(shape.num_layers)]
+        bt = torch.from_numpy(np.ascontiguousarray(w.block_tables)).cuda()
+        d_jobs = torch.from_numpy(jobs).cuda()
+        stream = torch.cuda.current_stream()
+        copy_stream = stream if k % 3 == 0 else torch.cuda.Stream()
+        with kv.KvPipeline(max_batches) as pl:
+            copy_stream.wait_stream(stream)
+            kv.kv_retrieve_pipelined(pl, lo, host, stg, layers, bt, w.bt_stride, w.num_reqs, jobs, d_jobs, spb,
+                                     copy_stream, stream)
+            torch.cuda.synchronize()
+        o_layers = [np.full(w.layer_bytes(), SENT_POOL, np.uint8) for _ in range(shape.num_layers)]
+        oracle.retrieve_scatter(olo, host.numpy().copy(), o_layers, w.block_tables, jobs)
+        for l in range(shape.num_layers):
+            assert np.array_equal(layers[l].cpu().numpy(), o_layers[l]), (k, shape, spb, max_batches, l)
+        named = set(int(x) for x in jobs[:, 0])
+        d, h = stg.cpu().numpy().reshape(S, sb), host.numpy().reshape(S, sb)
+        for x in range(S):
+            assert np.array_equal(d[x], h[x]) if x in named else np.all(d[x] == SENT_STG), (k, x)
+
+
 def test_retrieve_pipelined_empty_and_errors():
     w, lo, _ = _setup(71)
     sb, S = w.shape.slot_bytes, w.num_slots
