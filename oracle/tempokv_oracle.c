@@ -234,7 +234,7 @@ static int or_job_ok(const or_layout *lo, const or_job *jb, int32_t num_reqs, in
     int32_t nseg = lo->C / lo->B;
     if (jb->slot < 0 || jb->slot >= lo->num_slots) return 0;
     if (jb->req < 0 || jb->req >= num_reqs) return 0;
-    if (jb->chunk < 0 || (int64_t)(jb->chunk + 1) * nseg > bt_stride) return 0;
+    if (jb->chunk < 0 || ((int64_t)jb->chunk + 1) * nseg > bt_stride) return 0;
     return 1;
 }
 

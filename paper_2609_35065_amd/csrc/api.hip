@@ -227,7 +227,7 @@ int kv_validate_jobs(const kv_layout *layout, const int32_t *h_block_tables, int
     for (int32_t q = 0; q < num_jobs; ++q) {
         const kv_job &jb = h_jobs[q];
         if (jb.reserved != 0 || jb.slot < 0 || jb.slot >= layout->num_slots || jb.req < 0 || jb.req >= num_reqs ||
-            jb.chunk < 0 || (int64_t)(jb.chunk + 1) * nseg > bt_stride)
+            jb.chunk < 0 || ((int64_t)jb.chunk + 1) * nseg > bt_stride)
             return KV_ERANGE;
         for (int32_t i = 0; i < nseg; ++i) {
             const int32_t blk = h_block_tables[(int64_t)jb.req * bt_stride + (int64_t)jb.chunk * nseg + i];

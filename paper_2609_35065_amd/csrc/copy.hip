@@ -68,7 +68,7 @@ __device__ __forceinline__ v4u load16(const v4u *p) {
 
 __device__ __forceinline__ bool job_ok(const CopyParams &p, const v4i jb) {
     return jb.x >= 0 && jb.x < p.num_slots && jb.y >= 0 && jb.y < p.num_reqs && jb.z >= 0 &&
-           (int64_t)(jb.z + 1) * p.nseg <= p.bt_stride;
+           ((int64_t)jb.z + 1) * p.nseg <= p.bt_stride;
 }
 
 __device__ __forceinline__ bool blk_ok(const CopyParams &p, int32_t blk) {

@@ -131,7 +131,9 @@ def test_validate_jobs():
     assert kv.kv_validate_jobs(lo, bt, ok, True) == kv.KV_OK
     assert kv.kv_validate_jobs(lo, bt, np.array([[0, 0, 0, 0], [1, 0, 0, 0]], np.int32), False) == kv.KV_EDUP
     assert kv.kv_validate_jobs(lo, bt, np.array([[2, 0, 0, 0], [2, 1, 0, 0]], np.int32), True) == kv.KV_EDUP
-    for bad in ([4, 0, 0, 0], [-1, 0, 0, 0], [0, 2, 0, 0], [0, 0, 2, 0], [0, 0, -1, 0], [0, 0, 0, 1]):
+    # chunk = INT32_MAX: (chunk + 1) * C/B must be formed in 64 bits, or the bound check wraps and passes
+    for bad in ([4, 0, 0, 0], [-1, 0, 0, 0], [0, 2, 0, 0], [0, 0, 2, 0], [0, 0, -1, 0], [0, 0, 0, 1],
+                [0, 0, 0x7FFFFFFF, 0], [0, 1, 0x3FFFFFFF, 0]):
         assert kv.kv_validate_jobs(lo, bt, np.array([bad], np.int32), False) == kv.KV_ERANGE
     bt2 = bt.copy()
     bt2[0, 2] = 20

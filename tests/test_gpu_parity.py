@@ -344,8 +344,10 @@ def test_out_of_range_jobs_are_skipped_on_device():
     bt[0, 1] = -1
     bt[0, 2] = w.num_blocks + 5
     d_bt = torch.from_numpy(bt).cuda()
+    # chunk = INT32_MAX (and 2^30 - 1): the kernels form (chunk + 1) * C/B in 64 bits and skip the job
     jobs = np.array([[-1, 0, 0, 0], [w.num_slots, 0, 0, 0], [0, -1, 0, 0], [0, w.num_reqs, 0, 0],
-                     [0, 0, -1, 0], [0, 0, bt.shape[1], 0], [1, 0, 0, 0]], np.int32)
+                     [0, 0, -1, 0], [0, 0, bt.shape[1], 0], [0, 0, 0x7FFFFFFF, 0], [0, 1, 0x3FFFFFFF, 0],
+                     [1, 0, 0, 0]], np.int32)
     d_jobs = torch.from_numpy(jobs).cuda()
     kv.kv_retrieve_scatter(g.layout, g.staging, g.layers, d_bt, bt.shape[1], w.num_reqs, d_jobs, len(jobs))
     oracle.retrieve_scatter(o.layout, o.staging, o.layers, bt, jobs)

@@ -160,8 +160,9 @@ def test_out_of_range_jobs_and_blocks_touch_nothing():
     bt = bt.copy()
     bt[0, 1] = -1            # unassigned block
     bt[0, 2] = nb            # past the pool
+    # chunk = INT32_MAX: its end (chunk + 1) * C/B lies far past the table, however it is formed
     bad = np.array([[-1, 0, 0, 0], [6, 0, 0, 0], [0, -1, 0, 0], [0, 3, 0, 0],
-                    [0, 0, -1, 0], [0, 0, 3, 0]], np.int32)
+                    [0, 0, -1, 0], [0, 0, 3, 0], [0, 0, 0x7FFFFFFF, 0], [0, 1, 0x3FFFFFFF, 0]], np.int32)
     out = [a.copy() for a in layers]
     oracle.retrieve_scatter(lo, staging, out, bt, bad)
     assert all(np.array_equal(a, b) for a, b in zip(out, layers))

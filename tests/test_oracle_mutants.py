@@ -61,7 +61,7 @@ MUTANTS = [
      "                                int64_t src = jb->slot", "if (blk < 0 || blk > lo->num_blocks) continue;\n                    for (int32_t t = 0; t < lo->B; t++)\n"
      "                        for (int64_t x = 0; x < HD; x++)\n                            for (int32_t c = 0; c < lo->e; c++) {\n"
      "                                int64_t src = jb->slot"),
-    ("job_chunk_bound", COPY, "(int64_t)(jb->chunk + 1) * nseg > bt_stride", "(int64_t)jb->chunk * nseg > bt_stride"),
+    ("job_chunk_bound", COPY, "((int64_t)jb->chunk + 1) * nseg > bt_stride", "(int64_t)jb->chunk * nseg > bt_stride"),
     ("gather_kv_stride_dropped", COPY, "int64_t src = kv * lo->kv_stride + blk * lo->block_stride", "int64_t src = blk * lo->block_stride"),
     ("gather_segment_off_by_one", COPY, "+ ((((int64_t)l * 2 + kv) * lo->C + (int64_t)i * lo->B + t) * HD + x) * lo->e + c;\n"
      "                                int64_t src", "+ ((((int64_t)l * 2 + kv) * lo->C + (int64_t)(i + 1) % nseg * lo->B + t) * HD + x) * lo->e + c;\n"
