@@ -54,7 +54,8 @@ typedef enum kv_status {
     KV_ERANGE = -3,  /* slot, request, chunk or block id out of range (kv_validate_jobs) */
     KV_ENOSPC = -4,  /* no free staging slot for a miss, or the index is full */
     KV_EHIP = -5,    /* a HIP runtime call or kernel launch failed */
-    KV_EDUP = -6     /* two jobs of one batch write the same block (scatter) or slot (gather) */
+    KV_EDUP = -6,    /* two jobs of one batch write the same block (scatter) or slot (gather) */
+    KV_ELIMIT = -7   /* request larger than a fixed capacity (kv_index_insert_static) */
 } kv_status;
 
 /* Shapes and strides of the two KV layouts.
@@ -137,6 +138,26 @@ int kv_index_destroy(kv_index *idx);
  * one stay inserted), KV_EHIP. */
 int kv_index_insert(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slots, int32_t n,
                     void *stream);
+
+/* Allocation-free kv_index_insert, for callers that cannot allocate memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, host-table result and stream ordering as
+ * kv_index_insert, and it makes no hipMalloc, hipFree or other allocating
+ * call (its host-side change list and a rebuild of the host table use memory
+ * that kv_index_create reserved).  The (position, entry) pairs of an
+ * incremental device-table update are staged in a fixed device array of
+ * KV_INDEX_STATIC_MAX_PAIRS pairs (32 bytes each, 2 MiB) that the library
+ * holds on each GPU it runs on until the process ends, instead of in the
+ * index's own device lists; an update that changes more entries than the
+ * index's incremental limit sends the whole table image, which needs no
+ * staging.  Every call on one GPU shares that array and leaves the last
+ * call's pairs in it, so calls on one GPU must be ordered on one stream (or
+ * separated by a synchronisation): calls that overlap on one GPU race.
+ * Errors: those of kv_index_insert, and KV_ELIMIT (nothing inserted) when
+ * n > KV_INDEX_STATIC_MAX_PAIRS. */
+#define KV_INDEX_STATIC_MAX_PAIRS 65536
+int kv_index_insert_static(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slots, int32_t n,
+                           void *stream);
 
 /* Remove n keys (absent keys are ignored), then enqueue the device-table
  * update on `stream`. Errors: KV_EINVAL, KV_EHIP. */

@@ -18,7 +18,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtempokv.so")
 
-KV_OK, KV_EINVAL, KV_EALIGN, KV_ERANGE, KV_ENOSPC, KV_EHIP, KV_EDUP = 0, -1, -2, -3, -4, -5, -6
+KV_OK, KV_EINVAL, KV_EALIGN, KV_ERANGE, KV_ENOSPC, KV_EHIP, KV_EDUP, KV_ELIMIT = 0, -1, -2, -3, -4, -5, -6, -7
+KV_INDEX_STATIC_MAX_PAIRS = 65536
 KV_DEFER, KV_COMMIT, KV_BLOCKED, KV_ORDINARY = 0, 1, 2, 3
 KV_POLICY_DEMAND, KV_POLICY_IMMEDIATE, KV_POLICY_QUEUE_K, KV_POLICY_TEMPO_STATIC, KV_POLICY_TEMPO = range(5)
 KV_RETRIEVE_UNIT, KV_RETRIEVE_PAIR, KV_RETRIEVE_STREAM, KV_RETRIEVE_QUAD = range(4)
@@ -30,7 +31,8 @@ KV_MAX_LAYERS = 128
 HASH_BLOCK_TOKENS = 16
 
 # every symbol include/tempokv.h declares
-EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_erase",
+EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_insert", "kv_index_insert_static",
+           "kv_index_erase",
            "kv_index_size", "kv_index_find", "kv_lookup", "kv_build_jobs", "kv_retrieve_scatter",
            "kv_retrieve_plan", "kv_retrieve_scatter_as", "kv_store_gather", "kv_group_jobs_by_slot",
            "kv_validate_jobs", "kv_commit_should_stage", "kv_commit_should_stage_n", "kv_strerror",
@@ -89,6 +91,7 @@ def lib() -> ct.CDLL:
         "kv_index_create": [_i64, ct.POINTER(_vp)],
         "kv_index_destroy": [_vp],
         "kv_index_insert": [_vp, _vp, _vp, _i32, _vp],
+        "kv_index_insert_static": [_vp, _vp, _vp, _i32, _vp],
         "kv_index_erase": [_vp, _vp, _i32, _vp],
         "kv_index_size": [_vp, ct.POINTER(_i64)],
         "kv_index_find": [_vp, _u64, ct.POINTER(_i32)],
@@ -212,6 +215,9 @@ class KvIndex:
     def insert(self, keys: np.ndarray, slots: np.ndarray, stream=None) -> None:
         kv_index_insert(self, keys, slots, stream)
 
+    def insert_static(self, keys: np.ndarray, slots: np.ndarray, stream=None) -> None:
+        kv_index_insert_static(self, keys, slots, stream)
+
     def erase(self, keys: np.ndarray, stream=None) -> None:
         kv_index_erase(self, keys, stream)
 
@@ -248,6 +254,19 @@ def kv_index_insert(idx: KvIndex, keys: np.ndarray, slots: np.ndarray, stream=No
         raise ValueError("keys and slots differ in length")
     _check(lib().kv_index_insert(idx.handle, keys.ctypes.data, slots.ctypes.data, keys.size, _stream(stream)),
            "kv_index_insert")
+
+
+def kv_index_insert_static(idx: KvIndex, keys: np.ndarray, slots: np.ndarray, stream=None) -> None:
+    """kv_index_insert without any allocation: the device-table update is
+    staged in the library's fixed per-GPU array (at most
+    KV_INDEX_STATIC_MAX_PAIRS keys per call; calls on one GPU must be ordered
+    on one stream)."""
+    keys = np.ascontiguousarray(keys, np.uint64)
+    slots = np.ascontiguousarray(slots, np.int32)
+    if keys.size != slots.size:
+        raise ValueError("keys and slots differ in length")
+    _check(lib().kv_index_insert_static(idx.handle, keys.ctypes.data, slots.ctypes.data, keys.size,
+                                        _stream(stream)), "kv_index_insert_static")
 
 
 def kv_index_erase(idx: KvIndex, keys: np.ndarray, stream=None) -> None:

@@ -278,6 +278,7 @@ const char *kv_strerror(int status) {
     case KV_ENOSPC: return "no free staging slot or index full";
     case KV_EHIP: return "HIP runtime error";
     case KV_EDUP: return "duplicate destination within one batch";
+    case KV_ELIMIT: return "request exceeds a fixed capacity of the allocation-free call";
     default: return "unknown status";
     }
 }

@@ -17,6 +17,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -39,6 +40,7 @@ struct kv_index {
     int64_t live = 0;
     int64_t tombs = 0;
     std::vector<tkv::IndexEntry> host;
+    std::vector<tkv::IndexEntry> spare;   // same size as host: a rehash rebuilds into it, then swaps
     tkv::IndexEntry *dev = nullptr;
     tkv::IndexEntry *snap[2] = {nullptr, nullptr};
     tkv::IndexUpdate *dev_upd[2] = {nullptr, nullptr};
@@ -92,15 +94,16 @@ __global__ __launch_bounds__(kApplyThreads) void index_apply_kernel(const IndexU
     if (pos >= 0 && pos < cap) table[pos] = upd[i].entry;
 }
 
+// Rebuild the table without tombstones.  It uses the spare table reserved at
+// creation, so no host memory is allocated here.
 void rehash(kv_index *ix) {
     ix->full = true;
     ix->dirty.clear();
-    std::vector<IndexEntry> old;
-    old.swap(ix->host);
-    ix->host.assign(ix->cap, IndexEntry{0, -1, kEmpty});
+    ix->spare.swap(ix->host);
+    std::fill(ix->host.begin(), ix->host.end(), IndexEntry{0, -1, kEmpty});
     ix->tombs = 0;
     const uint64_t mask = (uint64_t)ix->cap - 1;
-    for (const IndexEntry &e : old) {
+    for (const IndexEntry &e : ix->spare) {
         if (e.state != kLive) continue;
         uint64_t pos = tkv::index_home(e.key, ix->log2cap);
         while (ix->host[pos].state != kEmpty) pos = (pos + 1) & mask;
@@ -108,7 +111,11 @@ void rehash(kv_index *ix) {
     }
 }
 
-int upload(kv_index *ix, hipStream_t stream) {
+// Mirror the host mutations since the last upload into the device table.  An
+// incremental update stages its (position, entry) pairs in `upd_list`, a
+// device buffer of `upd_pairs` pairs; more changes than that send the whole
+// table image.
+int upload_via(kv_index *ix, hipStream_t stream, IndexUpdate *upd_list, int64_t upd_pairs) {
     int prev = 0;
     if (hipGetDevice(&prev) != hipSuccess) return KV_EHIP;
     if (prev != ix->device && hipSetDevice(ix->device) != hipSuccess) return KV_EHIP;
@@ -119,7 +126,7 @@ int upload(kv_index *ix, hipStream_t stream) {
     std::sort(ix->dirty.begin(), ix->dirty.end());
     ix->dirty.erase(std::unique(ix->dirty.begin(), ix->dirty.end()), ix->dirty.end());
     const int64_t n = (int64_t)ix->dirty.size();
-    if (rc == KV_OK && (ix->full || n > ix->upd_cap)) {
+    if (rc == KV_OK && (ix->full || n > upd_pairs)) {
         memcpy(ix->snap[k], ix->host.data(), bytes);
         if (hipMemcpyAsync(ix->dev, ix->snap[k], bytes, hipMemcpyHostToDevice, stream) != hipSuccess ||
             hipEventRecord(ix->ev[k], stream) != hipSuccess)
@@ -130,12 +137,12 @@ int upload(kv_index *ix, hipStream_t stream) {
         IndexUpdate *list = reinterpret_cast<IndexUpdate *>(ix->snap[k]);
         for (int64_t i = 0; i < n; ++i) list[i] = IndexUpdate{ix->dirty[i], 0, ix->host[ix->dirty[i]]};
         (void)hipGetLastError();
-        if (hipMemcpyAsync(ix->dev_upd[k], list, sizeof(IndexUpdate) * (size_t)n, hipMemcpyHostToDevice, stream) !=
+        if (hipMemcpyAsync(upd_list, list, sizeof(IndexUpdate) * (size_t)n, hipMemcpyHostToDevice, stream) !=
             hipSuccess) {
             rc = KV_EHIP;
         } else {
             hipLaunchKernelGGL(index_apply_kernel, dim3((unsigned)((n + kApplyThreads - 1) / kApplyThreads)),
-                               dim3(kApplyThreads), 0, stream, ix->dev_upd[k], n, ix->cap, ix->dev);
+                               dim3(kApplyThreads), 0, stream, upd_list, n, ix->cap, ix->dev);
             if (hipGetLastError() != hipSuccess || hipEventRecord(ix->ev[k], stream) != hipSuccess)
                 rc = KV_EHIP;
             else
@@ -148,6 +155,66 @@ int upload(kv_index *ix, hipStream_t stream) {
     }
     ix->next = k ^ 1;
     if (prev != ix->device) (void)hipSetDevice(prev);
+    return rc;
+}
+
+int upload(kv_index *ix, hipStream_t stream) { return upload_via(ix, stream, ix->dev_upd[ix->next], ix->upd_cap); }
+
+// --------------------------------------------------------------------------
+// Allocation-free insert (kv_index_insert_static): the pairs of an
+// incremental update are staged in `scratch`, a fixed device array, instead
+// of the index's own device lists.  Each GPU holds its own copy of the array;
+// its address on a device is taken once, with that device current, and only
+// that address is handed to copies and kernels.  Every call on one GPU uses
+// the same array, so such calls must be ordered on one stream.
+// --------------------------------------------------------------------------
+constexpr int64_t kStaticPairs = KV_INDEX_STATIC_MAX_PAIRS;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) IndexUpdate scratch[kStaticPairs];
+
+std::mutex g_scratch_mu;
+IndexUpdate *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on `device`, which must be the current device,
+// or nullptr.  Taken once per device (by kv_index_create, the first call that
+// can need it there) and cached.
+IndexUpdate *scratch_on(int device) {
+    if (device < 0 || device >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        g_scratch_ptr[device] = static_cast<IndexUpdate *>(ptr);
+    }
+    return g_scratch_ptr[device];
+}
+
+// Host half of an insert: mutate the authoritative table and record the
+// changed positions.  Returns KV_OK or KV_ENOSPC (the pairs before the
+// failing one stay inserted).
+int insert_host(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slots, int32_t n) {
+    int rc = KV_OK;
+    for (int32_t i = 0; i < n; ++i) {
+        int64_t free_pos = -1;
+        const int64_t at = probe(idx, h_keys[i], &free_pos);
+        if (at >= 0) {
+            idx->host[at].slot = h_slots[i];
+            idx->dirty.push_back(at);
+            continue;
+        }
+        if (idx->live >= idx->max_entries || free_pos < 0) {
+            rc = KV_ENOSPC;
+            break;
+        }
+        if (idx->host[free_pos].state == kTomb) --idx->tombs;
+        idx->host[free_pos] = IndexEntry{h_keys[i], h_slots[i], kLive};
+        idx->dirty.push_back(free_pos);
+        ++idx->live;
+        if ((idx->live + idx->tombs) * 4 > idx->cap * 3) rehash(idx);
+    }
     return rc;
 }
 
@@ -185,6 +252,9 @@ int kv_index_create(int64_t max_entries, kv_index **out) {
     while ((int64_t(1) << ix->log2cap) < 2 * max_entries) ++ix->log2cap;
     ix->cap = int64_t(1) << ix->log2cap;
     ix->host.assign(ix->cap, IndexEntry{0, -1, kEmpty});
+    ix->spare.assign(ix->cap, IndexEntry{0, -1, kEmpty});
+    // changed positions between uploads: room for the largest allocation-free insert, and then some
+    ix->dirty.reserve(2 * (size_t)KV_INDEX_STATIC_MAX_PAIRS);
     const size_t bytes = sizeof(IndexEntry) * (size_t)ix->cap;
     // an incremental upload fits a snapshot buffer (cap entries = cap/2 pairs); past an eighth of the
     // table, or 65536 pairs, the whole image is sent instead
@@ -198,6 +268,7 @@ int kv_index_create(int64_t max_entries, kv_index **out) {
         hipHostMalloc((void **)&ix->snap[1], bytes, hipHostMallocDefault) != hipSuccess ||
         hipEventCreateWithFlags(&ix->ev[0], hipEventDisableTiming) != hipSuccess ||
         hipEventCreateWithFlags(&ix->ev[1], hipEventDisableTiming) != hipSuccess ||
+        !scratch_on(ix->device) ||   // set-up of kv_index_insert_static on this device
         hipDeviceSynchronize() != hipSuccess) {
         release(ix);
         return KV_EHIP;
@@ -216,26 +287,25 @@ int kv_index_insert(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slot
     if (!idx || n < 0 || (n > 0 && (!h_keys || !h_slots))) return KV_EINVAL;
     for (int32_t i = 0; i < n; ++i)
         if (h_slots[i] < 0) return KV_EINVAL;
-    int rc = KV_OK;
-    for (int32_t i = 0; i < n; ++i) {
-        int64_t free_pos = -1;
-        const int64_t at = probe(idx, h_keys[i], &free_pos);
-        if (at >= 0) {
-            idx->host[at].slot = h_slots[i];
-            idx->dirty.push_back(at);
-            continue;
-        }
-        if (idx->live >= idx->max_entries || free_pos < 0) {
-            rc = KV_ENOSPC;
-            break;
-        }
-        if (idx->host[free_pos].state == kTomb) --idx->tombs;
-        idx->host[free_pos] = IndexEntry{h_keys[i], h_slots[i], kLive};
-        idx->dirty.push_back(free_pos);
-        ++idx->live;
-        if ((idx->live + idx->tombs) * 4 > idx->cap * 3) rehash(idx);
-    }
+    const int rc = insert_host(idx, h_keys, h_slots, n);
     const int up = upload(idx, (hipStream_t)stream);
+    return rc != KV_OK ? rc : up;
+}
+
+int kv_index_insert_static(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slots, int32_t n,
+                           void *stream) {
+    if (!idx || n < 0 || (n > 0 && (!h_keys || !h_slots))) return KV_EINVAL;
+    if (n > kStaticPairs) return KV_ELIMIT;
+    for (int32_t i = 0; i < n; ++i)
+        if (h_slots[i] < 0) return KV_EINVAL;
+    int prev = 0;
+    if (hipGetDevice(&prev) != hipSuccess) return KV_EHIP;
+    if (prev != idx->device && hipSetDevice(idx->device) != hipSuccess) return KV_EHIP;
+    IndexUpdate *list = scratch_on(idx->device);
+    if (prev != idx->device) (void)hipSetDevice(prev);
+    if (!list) return KV_EHIP;
+    const int rc = insert_host(idx, h_keys, h_slots, n);
+    const int up = upload_via(idx, (hipStream_t)stream, list, std::min<int64_t>(idx->upd_cap, kStaticPairs));
     return rc != KV_OK ? rc : up;
 }
 
