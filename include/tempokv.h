@@ -13,7 +13,9 @@
  *   kv_retrieve_scatter   staged chunk [L,2,C,H,D] -> paged KV blocks (one launch;
  *                         kv_retrieve_plan / kv_retrieve_scatter_as pick a variant)
  *   kv_store_gather       paged KV blocks -> staged chunk (one launch)
- *   kv_commit_should_stage  the TTU/TTR commitment rule of Section 3.2 (host)
+ *   kv_commit_should_stage  the TTU/TTR commitment rule of Section 3.2 (host);
+ *                         kv_decide_claims / kv_build_jobs_routed apply it to a
+ *                         batch and route each claim; kv_ttr_* estimate TTR
  *   kv_stage_in / kv_retrieve_pipelined  lower tier -> HBM staging, and the
  *                         retrieve gated on those copies (stage-ready)
  *   kv_sim_run            claim/commitment controller in a discrete-event
@@ -184,6 +186,14 @@ int kv_lookup(const kv_index *idx, const uint64_t *d_block_hash, const int64_t *
 /* ----------------------------------------------------------------------- */
 /* Host job build                                                           */
 /* ----------------------------------------------------------------------- */
+
+/* Chunk keys of a batch from its block hashes (host arrays): for request r
+ * and chunk j < floor(nb_r / blocks_per_chunk),
+ *     h_keys[h_chunk_off[r] + j] = h_block_hash[h_blk_off[r] + (j+1)*blocks_per_chunk - 1],
+ * the key kv_lookup probes (the hash at the chunk's last block).  Errors:
+ * KV_EINVAL (null pointer, offsets inconsistent with blocks_per_chunk). */
+int kv_chunk_keys(const uint64_t *h_block_hash, const int64_t *h_blk_off, int32_t num_reqs,
+                  int32_t blocks_per_chunk, const int64_t *h_chunk_off, uint64_t *h_keys);
 
 /* Turn a lookup result (copied to the host) into transfer jobs.
  *   retrieve jobs: {chunk_slot, r, j} for every j < h_hit_chunks[r], in (r, j)
@@ -373,6 +383,74 @@ int kv_commit_should_stage(double ttu_s, double ttr_s, uint64_t free_protected_b
 int kv_commit_should_stage_n(int32_t n, const double *h_ttu, const double *h_ttr, uint64_t free_protected_bytes,
                              const uint64_t *h_claim_new, const uint64_t *h_claim_total, uint64_t budget_bytes,
                              const uint8_t *h_requested, int32_t *h_out);
+
+/* Commitment decisions for the claims of one batch (Section 3.2).  Claim r
+ * is the matched prefix of request r: its KV objects are the distinct staging
+ * slots h_chunk_slot[h_chunk_off[r] + j], j < h_hit_chunks[r] (as a lookup
+ * leaves them), slot_bytes bytes each.  Claims are evaluated in the order of
+ * "Commitment and replanning": those with a pending retrieval request
+ * (h_requested[r] != 0) first, then the others, each group in request order;
+ * a claim that cannot commit does not block the ones after it.  For each claim
+ *   total = its objects x slot_bytes,  new = bytes of its objects not yet
+ *   protected (h_protected[slot] == 0),  free = budget_bytes - *reserved_bytes
+ *   (0 when the reservations exceed the budget),
+ *   h_decision[r] = kv_commit_should_stage(h_ttu[r], h_ttr[r], free, new,
+ *                                          total, budget_bytes, h_requested[r]).
+ * A KV_COMMIT protects the claim's objects and adds `new` to *reserved_bytes:
+ * objects shared by claims are reserved once ("Shared staging and resource
+ * lifecycle").  h_protected (uint8 [num_slots]) and *reserved_bytes are the
+ * protected-capacity ledger, read and updated in place; start them at zero
+ * when no earlier commitment is still in force.  Host arrays only.  Errors:
+ * KV_EINVAL (null pointer, inconsistent offsets or hit counts), KV_ERANGE (a
+ * matched slot outside [0, num_slots)); a claim with a NaN estimate gets
+ * KV_EINVAL as its decision. */
+int kv_decide_claims(int32_t num_reqs, const int32_t *h_hit_chunks, const int32_t *h_chunk_slot,
+                     const int64_t *h_chunk_off, const double *h_ttu, const double *h_ttr,
+                     const uint8_t *h_requested, uint64_t slot_bytes, uint64_t budget_bytes, int64_t num_slots,
+                     uint8_t *h_protected, uint64_t *reserved_bytes, int32_t *h_decision);
+
+/* kv_build_jobs for a batch whose claims were decided (kv_decide_claims).
+ * Only requests whose retrieval is requested (h_requested[r] != 0) run in
+ * this batch and get jobs; the others have none yet.  A running request's
+ * matched chunks become retrieve jobs in h_retrieve when its decision is
+ * KV_COMMIT (the protected, staged route) and in h_ordinary when it is
+ * KV_ORDINARY (the ordinary retrieval path, "Protected capacity and on-demand
+ * retrieval"); its store jobs follow the rule of kv_build_jobs over the
+ * running requests only.  h_ordinary must hold h_chunk_off[num_reqs] jobs
+ * like the other two lists.  Errors: those of kv_build_jobs, and KV_EINVAL
+ * for a running request whose decision is neither KV_COMMIT nor KV_ORDINARY. */
+int kv_build_jobs_routed(const int32_t *h_hit_chunks, const int32_t *h_chunk_slot,
+                         const uint64_t *h_block_hash, const int64_t *h_blk_off, const int64_t *h_chunk_off,
+                         int32_t num_reqs, int32_t blocks_per_chunk, const int32_t *h_free_slots,
+                         int32_t num_free, const uint8_t *h_requested, const int32_t *h_decision,
+                         kv_job *h_retrieve, int32_t *num_retrieve, kv_job *h_ordinary, int32_t *num_ordinary,
+                         kv_job *h_store, uint64_t *h_store_keys, int32_t *num_store, int32_t *dropped);
+
+/* ----------------------------------------------------------------------- */
+/* Time-to-ready estimates (host)                                           */
+/* ----------------------------------------------------------------------- */
+
+/* The two TTR estimators of Section 3.1 ("Storage-estimated time-to-ready")
+ * and Section 5 ("Policies"), over the distinct KV objects h_objs[0..n) of one
+ * claim (ids below num_objects; per-object arrays are indexed by id).  They
+ * feed kv_commit_should_stage, and the simulator (kv_sim_run) uses the same
+ * code.
+ * Static (TempoKV-Static): the claim's non-resident bytes over a fixed rate,
+ * as if the claim were staged in isolation:
+ *     *ttr_s = sum over non-resident o of h_obj_bytes[o] / static_rate. */
+int kv_ttr_static(int32_t n, const int32_t *h_objs, int32_t num_objects, const double *h_obj_bytes,
+                  const uint8_t *h_resident, double static_rate, double *ttr_s);
+
+/* State-aware: the staging device's queue projected from now_s.  An object
+ * already queued (h_queued[o] != 0) becomes resident at h_ready_at[o]; each
+ * non-resident object not yet queued is appended, in claim order, behind the
+ * queue's tail max(busy_until_s, now_s) at stage_rate bytes/s; the claim is
+ * ready when its last object is: *ttr_s = (latest such time, at least now_s)
+ * - now_s.  Errors (both): KV_EINVAL for a null pointer, an object id out of
+ * range, a rate <= 0 or a NaN time. */
+int kv_ttr_state_aware(int32_t n, const int32_t *h_objs, int32_t num_objects, const double *h_obj_bytes,
+                       const uint8_t *h_resident, const uint8_t *h_queued, const double *h_ready_at,
+                       double now_s, double busy_until_s, double stage_rate, double *ttr_s);
 
 /* ----------------------------------------------------------------------- */
 /* Claim controller and staging simulator (host)                            */

@@ -75,6 +75,11 @@ def lib() -> ct.CDLL:
                                       ct.c_int32, i32p, ct.c_int32]
     L.or_store_gather.restype = None
     L.or_store_gather.argtypes = L.or_retrieve_scatter.argtypes
+    L.or_retrieve_scatter_layer.restype = None
+    L.or_retrieve_scatter_layer.argtypes = [ct.POINTER(OrLayout), u8p, u8p, i32p, ct.c_int32, ct.c_int32, i32p,
+                                            ct.c_int32]
+    L.or_store_gather_layer.restype = None
+    L.or_store_gather_layer.argtypes = L.or_retrieve_scatter_layer.argtypes
     L.or_scatter_source.restype = ct.c_int
     L.or_scatter_source.argtypes = [ct.POINTER(OrLayout), i32p, ct.c_int32, ct.c_int32, i32p, ct.c_int32,
                                     ct.c_int32, ct.c_int32, ct.c_int64, i64p]
@@ -223,6 +228,40 @@ def store_gather(layout: OrLayout, staging: np.ndarray, layers: Sequence[np.ndar
     lib().or_store_gather(ct.byref(layout), staging.ctypes.data_as(ct.POINTER(ct.c_uint8)),
                           _layer_array(layers), _p(bt, ct.c_int32), bt.shape[1], bt.shape[0],
                           _p(jb, ct.c_int32), len(jobs))
+
+
+def layer_part_bytes(layout: OrLayout) -> int:
+    """Bytes of one layer of one staging slot ([2][C][H][D] elements)."""
+    return 2 * layout.C * layout.H * layout.D * layout.e
+
+
+def retrieve_scatter_layer(layout: OrLayout, stg_layer: np.ndarray, paged: np.ndarray,
+                           block_tables: np.ndarray, jobs: np.ndarray) -> None:
+    """In place: one layer's paged tensor receives that layer's part of the
+    staged chunks of ``jobs``; ``stg_layer`` holds the layer's part of every
+    slot back to back (slot s at s * layer_part_bytes)."""
+    bt = np.ascontiguousarray(block_tables, np.int32)
+    jb = np.ascontiguousarray(jobs if len(jobs) else np.zeros((1, 4)), np.int32)
+    assert stg_layer.dtype == np.uint8 and stg_layer.flags.c_contiguous
+    assert stg_layer.size >= layout.num_slots * layer_part_bytes(layout)
+    assert paged.dtype == np.uint8 and paged.flags.c_contiguous
+    lib().or_retrieve_scatter_layer(ct.byref(layout), stg_layer.ctypes.data_as(ct.POINTER(ct.c_uint8)),
+                                    paged.ctypes.data_as(ct.POINTER(ct.c_uint8)), _p(bt, ct.c_int32), bt.shape[1],
+                                    bt.shape[0], _p(jb, ct.c_int32), len(jobs))
+
+
+def store_gather_layer(layout: OrLayout, stg_layer: np.ndarray, paged: np.ndarray,
+                       block_tables: np.ndarray, jobs: np.ndarray) -> None:
+    """In place: ``stg_layer`` (one layer's part of every slot) receives that
+    layer's paged blocks of ``jobs``."""
+    bt = np.ascontiguousarray(block_tables, np.int32)
+    jb = np.ascontiguousarray(jobs if len(jobs) else np.zeros((1, 4)), np.int32)
+    assert stg_layer.dtype == np.uint8 and stg_layer.flags.c_contiguous
+    assert stg_layer.size >= layout.num_slots * layer_part_bytes(layout)
+    assert paged.dtype == np.uint8 and paged.flags.c_contiguous
+    lib().or_store_gather_layer(ct.byref(layout), stg_layer.ctypes.data_as(ct.POINTER(ct.c_uint8)),
+                                paged.ctypes.data_as(ct.POINTER(ct.c_uint8)), _p(bt, ct.c_int32), bt.shape[1],
+                                bt.shape[0], _p(jb, ct.c_int32), len(jobs))
 
 
 def scatter_source(layout: OrLayout, block_tables: np.ndarray, jobs: np.ndarray,

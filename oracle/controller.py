@@ -101,6 +101,31 @@ class SimConfig:
     queue_k: int = 4
 
 
+def ttr_static_of(objs, obj_bytes, resident, static_rate):
+    """Static TTR (Section 5, TempoKV-Static): the claim's non-resident bytes
+    over a fixed staging rate, as if it were staged alone."""
+    return sum(obj_bytes[o] for o in objs if not resident[o]) / static_rate
+
+
+def ttr_state_aware_of(objs, obj_bytes, resident, queued, ready_at, now, busy_until, stage_rate):
+    """State-aware TTR (Section 3.1, "Storage-estimated time-to-ready"): the
+    staging queue projected from `now`.  Objects already queued keep their
+    completion times; the claim's other non-resident objects are appended, in
+    claim order, behind the queue's tail at the aggregate staging rate; the
+    last object to become resident decides."""
+    t_end = now
+    tail = max(busy_until, now)
+    for o in objs:
+        if resident[o]:
+            continue
+        if queued[o]:
+            t_end = max(t_end, ready_at[o])
+        else:
+            tail = tail + obj_bytes[o] / stage_rate
+            t_end = max(t_end, tail)
+    return t_end - now
+
+
 def simulate(cfg: SimConfig, obj_bytes: Sequence[float], arrival: Sequence[float],
              manifests: Sequence[Sequence[int]], uncached: Sequence[int], out_tokens: Sequence[int]) -> Dict:
     N, O = len(arrival), len(obj_bytes)
@@ -163,20 +188,10 @@ def simulate(cfg: SimConfig, obj_bytes: Sequence[float], arrival: Sequence[float
             lru[o] = now
 
     def ttr_static(i):
-        return sum(obj_bytes[o] for o in uniq[i] if not resident[o]) / cfg.static_rate
+        return ttr_static_of(uniq[i], obj_bytes, resident, cfg.static_rate)
 
     def ttr_state(i):
-        t_end = now
-        tail = max(busy_until, now)
-        for o in uniq[i]:
-            if resident[o]:
-                continue
-            if queued[o]:
-                t_end = max(t_end, ready_at[o])
-            else:
-                tail = tail + obj_bytes[o] / cfg.stage_rate
-                t_end = max(t_end, tail)
-        return t_end - now
+        return ttr_state_aware_of(uniq[i], obj_bytes, resident, queued, ready_at, now, busy_until, cfg.stage_rate)
 
     def projected_end(i):
         if phase[i] == PH_RUN:

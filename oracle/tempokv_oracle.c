@@ -303,6 +303,68 @@ void or_store_gather(const or_layout *lo, uint8_t *staging, const uint8_t *const
     }
 }
 
+/* One-layer forms of the two copies, for complete checks of buffers too large
+ * to hold on the host at once: the walk of or_retrieve_scatter and
+ * or_store_gather for the single layer `layer`, with the staging side given
+ * as that layer's part of every slot, back to back:
+ *   stg_layer byte s*(2*C*H*D*e) + ((kv*C + i*B + t)*H*D + x)*e + c
+ *     is staging byte s*slot_bytes + (((layer*2 + kv)*C + i*B + t)*H*D + x)*e + c
+ * and `paged` that layer's paged tensor.  The job and block checks are those
+ * of the full walks. */
+void or_retrieve_scatter_layer(const or_layout *lo, const uint8_t *stg_layer, uint8_t *paged,
+                               const int32_t *bt, int32_t bt_stride, int32_t num_reqs,
+                               const or_job *jobs, int32_t num_jobs)
+{
+    int64_t HD = (int64_t)lo->H * lo->D;
+    int64_t part_bytes = (int64_t)2 * lo->C * HD * lo->e;    /* one layer of one slot */
+    int32_t nseg = lo->C / lo->B;
+    for (int32_t q = 0; q < num_jobs; q++) {
+        const or_job *jb = &jobs[q];
+        if (!or_job_ok(lo, jb, num_reqs, bt_stride)) continue;
+        for (int32_t kv = 0; kv < 2; kv++)
+            for (int32_t i = 0; i < nseg; i++) {
+                int32_t blk = bt[(int64_t)jb->req * bt_stride + (int64_t)jb->chunk * nseg + i];
+                if (blk < 0 || blk >= lo->num_blocks) continue;
+                for (int32_t t = 0; t < lo->B; t++)
+                    for (int64_t x = 0; x < HD; x++)
+                        for (int32_t c = 0; c < lo->e; c++) {
+                            int64_t src = jb->slot * part_bytes
+                                + (((int64_t)kv * lo->C + (int64_t)i * lo->B + t) * HD + x) * lo->e + c;
+                            int64_t dst = kv * lo->kv_stride + blk * lo->block_stride
+                                + ((int64_t)t * HD + x) * lo->e + c;
+                            paged[dst] = stg_layer[src];
+                        }
+            }
+    }
+}
+
+void or_store_gather_layer(const or_layout *lo, uint8_t *stg_layer, const uint8_t *paged,
+                           const int32_t *bt, int32_t bt_stride, int32_t num_reqs,
+                           const or_job *jobs, int32_t num_jobs)
+{
+    int64_t HD = (int64_t)lo->H * lo->D;
+    int64_t part_bytes = (int64_t)2 * lo->C * HD * lo->e;
+    int32_t nseg = lo->C / lo->B;
+    for (int32_t q = 0; q < num_jobs; q++) {
+        const or_job *jb = &jobs[q];
+        if (!or_job_ok(lo, jb, num_reqs, bt_stride)) continue;
+        for (int32_t kv = 0; kv < 2; kv++)
+            for (int32_t i = 0; i < nseg; i++) {
+                int32_t blk = bt[(int64_t)jb->req * bt_stride + (int64_t)jb->chunk * nseg + i];
+                if (blk < 0 || blk >= lo->num_blocks) continue;
+                for (int32_t t = 0; t < lo->B; t++)
+                    for (int64_t x = 0; x < HD; x++)
+                        for (int32_t c = 0; c < lo->e; c++) {
+                            int64_t dst = jb->slot * part_bytes
+                                + (((int64_t)kv * lo->C + (int64_t)i * lo->B + t) * HD + x) * lo->e + c;
+                            int64_t src = kv * lo->kv_stride + blk * lo->block_stride
+                                + ((int64_t)t * HD + x) * lo->e + c;
+                            stg_layer[dst] = paged[src];
+                        }
+            }
+    }
+}
+
 /* One-by-one forms of the two copies, for sampled checks on buffers too large
  * to hold twice on the host.  They scan the job list in order; the last job
  * that reaches the asked-for location decides (with disjoint destinations,

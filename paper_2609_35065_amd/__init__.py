@@ -37,7 +37,12 @@ EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_in
            "kv_retrieve_plan", "kv_retrieve_scatter_as", "kv_store_gather", "kv_group_jobs_by_slot",
            "kv_validate_jobs", "kv_commit_should_stage", "kv_commit_should_stage_n", "kv_strerror",
            "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out",
-           "kv_pipeline_create", "kv_pipeline_destroy", "kv_retrieve_pipelined"]
+           "kv_pipeline_create", "kv_pipeline_destroy", "kv_retrieve_pipelined", "kv_decide_claims",
+           "kv_build_jobs_routed", "kv_ttr_static", "kv_ttr_state_aware", "kv_chunk_keys"]
+# the calls that run on the host only (host.cpp, controller.cpp)
+HOST_CALLS = ["kv_build_jobs", "kv_build_jobs_routed", "kv_decide_claims", "kv_group_jobs_by_slot",
+              "kv_validate_jobs", "kv_commit_should_stage", "kv_commit_should_stage_n", "kv_retrieve_plan",
+              "kv_strerror", "kv_version", "kv_sim_run", "kv_ttr_static", "kv_ttr_state_aware", "kv_chunk_keys"]
 
 
 class KvError(RuntimeError):
@@ -71,7 +76,62 @@ class KvSimEvent(ct.Structure):
 
 
 _lib: Optional[ct.CDLL] = None
+# Tests only: a separately built copy of the host-only calls (HOST_CALLS) from the same sources, e.g. a
+# sanitizer build, used by the host-call wrappers in place of libtempokv.so.
+_host_override: Optional[ct.CDLL] = None
 _vp, _i32, _i64, _u64, _dbl = ct.c_void_p, ct.c_int32, ct.c_int64, ct.c_uint64, ct.c_double
+
+SIGNATURES = {
+    "kv_hash_prefix": [_vp, _vp, _i32, _u64, _vp, _vp, _vp],
+    "kv_index_create": [_i64, ct.POINTER(_vp)],
+    "kv_index_destroy": [_vp],
+    "kv_index_insert": [_vp, _vp, _vp, _i32, _vp],
+    "kv_index_insert_static": [_vp, _vp, _vp, _i32, _vp],
+    "kv_index_erase": [_vp, _vp, _i32, _vp],
+    "kv_index_size": [_vp, ct.POINTER(_i64)],
+    "kv_index_find": [_vp, _u64, ct.POINTER(_i32)],
+    "kv_lookup": [_vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp],
+    "kv_build_jobs": [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, ct.POINTER(_i32), _vp, _vp,
+                      ct.POINTER(_i32), ct.POINTER(_i32)],
+    "kv_build_jobs_routed": [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, _vp, _vp, ct.POINTER(_i32), _vp,
+                             ct.POINTER(_i32), _vp, _vp, ct.POINTER(_i32), ct.POINTER(_i32)],
+    "kv_chunk_keys": [_vp, _vp, _i32, _i32, _vp, _vp],
+    "kv_decide_claims": [_i32, _vp, _vp, _vp, _vp, _vp, _vp, _u64, _u64, _i64, _vp, ct.POINTER(_u64), _vp],
+    "kv_retrieve_scatter": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
+    "kv_store_gather": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
+    "kv_retrieve_plan": [ct.POINTER(KvLayout), _vp, _i32],
+    "kv_retrieve_scatter_as": [_i32, ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
+    "kv_group_jobs_by_slot": [_vp, _i32],
+    "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
+    "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
+    "kv_commit_should_stage_n": [_i32, _vp, _vp, _u64, _vp, _vp, _u64, _vp, _vp],
+    "kv_ttr_static": [_i32, _vp, _i32, _vp, _vp, _dbl, ct.POINTER(_dbl)],
+    "kv_ttr_state_aware": [_i32, _vp, _i32, _vp, _vp, _vp, _vp, _dbl, _dbl, _dbl, ct.POINTER(_dbl)],
+    "kv_strerror": [ct.c_int],
+    "kv_host_device_pointer": [_vp, ct.POINTER(_vp)],
+    "kv_version": [],
+    "kv_sim_run": [ct.POINTER(KvSimConfig), _vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp,
+                   ct.POINTER(KvSimResult), _vp, _i64, ct.POINTER(_i64)],
+    "kv_stage_in": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _vp],
+    "kv_stage_out": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _vp],
+    "kv_pipeline_create": [_i32, ct.POINTER(_vp)],
+    "kv_pipeline_destroy": [_vp],
+    "kv_retrieve_pipelined": [_vp, ct.POINTER(KvLayout), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _i32, _i32,
+                              _vp, _vp],
+}
+
+
+def declare(L: ct.CDLL, names) -> ct.CDLL:
+    """Set the argument and result types of the named calls on a loaded library."""
+    for name in names:
+        f = getattr(L, name)
+        f.argtypes = SIGNATURES[name]
+        f.restype = ct.c_int
+    if "kv_strerror" in names:
+        L.kv_strerror.restype = ct.c_char_p
+    if "kv_version" in names:
+        L.kv_version.restype = ct.c_char_p
+    return L
 
 
 def lib() -> ct.CDLL:
@@ -85,55 +145,22 @@ def lib() -> ct.CDLL:
     # torch first: the library then binds to the HIP runtime torch already
     # loaded (same soname), so torch's streams and allocations are its own.
     import torch  # noqa: F401
-    L = ct.CDLL(LIB_PATH)
-    sig = {
-        "kv_hash_prefix": [_vp, _vp, _i32, _u64, _vp, _vp, _vp],
-        "kv_index_create": [_i64, ct.POINTER(_vp)],
-        "kv_index_destroy": [_vp],
-        "kv_index_insert": [_vp, _vp, _vp, _i32, _vp],
-        "kv_index_insert_static": [_vp, _vp, _vp, _i32, _vp],
-        "kv_index_erase": [_vp, _vp, _i32, _vp],
-        "kv_index_size": [_vp, ct.POINTER(_i64)],
-        "kv_index_find": [_vp, _u64, ct.POINTER(_i32)],
-        "kv_lookup": [_vp, _vp, _vp, _i32, _i32, _vp, _vp, _vp, _vp],
-        "kv_build_jobs": [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, ct.POINTER(_i32), _vp, _vp,
-                          ct.POINTER(_i32), ct.POINTER(_i32)],
-        "kv_retrieve_scatter": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
-        "kv_store_gather": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
-        "kv_retrieve_plan": [ct.POINTER(KvLayout), _vp, _i32],
-        "kv_retrieve_scatter_as": [_i32, ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
-        "kv_group_jobs_by_slot": [_vp, _i32],
-        "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
-        "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
-        "kv_commit_should_stage_n": [_i32, _vp, _vp, _u64, _vp, _vp, _u64, _vp, _vp],
-        "kv_strerror": [ct.c_int],
-        "kv_host_device_pointer": [_vp, ct.POINTER(_vp)],
-        "kv_version": [],
-        "kv_sim_run": [ct.POINTER(KvSimConfig), _vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp,
-                       ct.POINTER(KvSimResult), _vp, _i64, ct.POINTER(_i64)],
-        "kv_stage_in": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _vp],
-        "kv_stage_out": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _vp],
-        "kv_pipeline_create": [_i32, ct.POINTER(_vp)],
-        "kv_pipeline_destroy": [_vp],
-        "kv_retrieve_pipelined": [_vp, ct.POINTER(KvLayout), _vp, _vp, _vp, _vp, _i32, _i32, _vp, _vp, _i32, _i32,
-                                  _vp, _vp],
-    }
-    for name, args in sig.items():
-        f = getattr(L, name)
-        f.argtypes = args
-        f.restype = ct.c_int
-    L.kv_strerror.restype = ct.c_char_p
-    L.kv_version.restype = ct.c_char_p
-    _lib = L
-    return L
+    _lib = declare(ct.CDLL(LIB_PATH), list(SIGNATURES))
+    return _lib
+
+
+def host_lib() -> ct.CDLL:
+    """The library whose host-only calls the wrappers below use: libtempokv.so,
+    unless a test installed a separately built copy of those calls."""
+    return _host_override if _host_override is not None else lib()
 
 
 def strerror(status: int) -> str:
-    return lib().kv_strerror(status).decode()
+    return host_lib().kv_strerror(status).decode()
 
 
 def kv_version() -> str:
-    return lib().kv_version().decode()
+    return host_lib().kv_version().decode()
 
 
 def _check(rc: int, what: str) -> int:
@@ -167,12 +194,6 @@ def _dptr(t, dtype=None, what: str = "tensor") -> int:
     if dtype is not None and t.dtype != dtype:
         raise ValueError(f"{what} must be {dtype}, got {t.dtype}")
     return t.data_ptr()
-
-
-def _hptr(a: np.ndarray, dtype, what: str):
-    if not isinstance(a, np.ndarray) or a.dtype != dtype or not a.flags.c_contiguous:
-        raise ValueError(f"{what} must be a contiguous numpy {np.dtype(dtype)} array")
-    return a.ctypes.data
 
 
 def make_layout(num_layers: int, kv_heads: int, head_dim: int, elem_bytes: int, block_size: int,
@@ -310,12 +331,113 @@ def kv_build_jobs(hit_chunks: np.ndarray, chunk_slot: np.ndarray, block_hash: np
     store = np.zeros((max(nchunks, 1), 4), np.int32)
     keys = np.zeros(max(nchunks, 1), np.uint64)
     nr, ns, nd = _i32(0), _i32(0), _i32(0)
-    rc = lib().kv_build_jobs(hit.ctypes.data, cs.ctypes.data, bh.ctypes.data, bo.ctypes.data, co.ctypes.data, R,
+    rc = host_lib().kv_build_jobs(hit.ctypes.data, cs.ctypes.data, bh.ctypes.data, bo.ctypes.data, co.ctypes.data, R,
                              blocks_per_chunk, fs.ctypes.data if fs.size else None, fs.size, retr.ctypes.data,
                              ct.byref(nr), store.ctypes.data, keys.ctypes.data, ct.byref(ns), ct.byref(nd))
     if rc < 0 and rc != KV_ENOSPC:
         raise KvError(rc, "kv_build_jobs")
     return retr[:nr.value].copy(), store[:ns.value].copy(), keys[:ns.value].copy(), nd.value, rc
+
+
+def kv_chunk_keys(block_hash: np.ndarray, blk_off: np.ndarray, blocks_per_chunk: int,
+                  chunk_off: np.ndarray) -> np.ndarray:
+    """Chunk keys (uint64, in (request, chunk) order) from host block hashes."""
+    R = blk_off.size - 1
+    bh = np.ascontiguousarray(block_hash if np.size(block_hash) else np.zeros(1), np.uint64)
+    bo = np.ascontiguousarray(blk_off, np.int64)
+    co = np.ascontiguousarray(chunk_off, np.int64)
+    out = np.zeros(max(int(co[-1]) if co.size else 0, 1), np.uint64)
+    _check(host_lib().kv_chunk_keys(bh.ctypes.data, bo.ctypes.data, R, blocks_per_chunk,
+                                    co.ctypes.data, out.ctypes.data), "kv_chunk_keys")
+    return out[:int(co[-1]) if co.size else 0].copy()
+
+
+def kv_decide_claims(hit_chunks: np.ndarray, chunk_slot: np.ndarray, chunk_off: np.ndarray, ttu, ttr, requested,
+                     slot_bytes: int, budget_bytes: int, num_slots: int, protected: Optional[np.ndarray] = None,
+                     reserved_bytes: int = 0):
+    """Commitment decisions for the claims of a batch.  Returns (decisions
+    int32 [R], protected uint8 [num_slots], reserved bytes); `protected` and
+    `reserved_bytes` are the ledger to start from (default: nothing
+    protected)."""
+    R = chunk_off.size - 1
+    hit = np.ascontiguousarray(hit_chunks, np.int32)
+    cs = np.ascontiguousarray(chunk_slot, np.int32)
+    co = np.ascontiguousarray(chunk_off, np.int64)
+    u = np.ascontiguousarray(np.broadcast_to(np.asarray(ttu, np.float64), (R,)))
+    t = np.ascontiguousarray(np.broadcast_to(np.asarray(ttr, np.float64), (R,)))
+    rq = np.ascontiguousarray(np.broadcast_to(np.asarray(requested).astype(bool), (R,)), np.uint8)
+    prot = (np.zeros(num_slots, np.uint8) if protected is None
+            else np.ascontiguousarray(protected, np.uint8).copy())
+    if prot.size != num_slots:
+        raise ValueError("protected must hold one flag per staging slot")
+    dec = np.zeros(max(R, 1), np.int32)
+    res = _u64(int(reserved_bytes))
+    _check(host_lib().kv_decide_claims(R, hit.ctypes.data, cs.ctypes.data, co.ctypes.data, u.ctypes.data,
+                                       t.ctypes.data, rq.ctypes.data, int(slot_bytes), int(budget_bytes),
+                                       int(num_slots), prot.ctypes.data, ct.byref(res), dec.ctypes.data),
+           "kv_decide_claims")
+    return dec[:R].copy(), prot, res.value
+
+
+def kv_build_jobs_routed(hit_chunks: np.ndarray, chunk_slot: np.ndarray, block_hash: np.ndarray,
+                         blk_off: np.ndarray, chunk_off: np.ndarray, blocks_per_chunk: int, free_slots: np.ndarray,
+                         requested, decisions: np.ndarray):
+    """Returns (retrieve [n,4], ordinary [k,4], store [m,4], store_keys [m], dropped, status): the jobs of
+    the requests whose retrieval is requested, their matched chunks split by commitment decision."""
+    R = blk_off.size - 1
+    nchunks = int(chunk_off[-1]) if chunk_off.size else 0
+    hit = np.ascontiguousarray(hit_chunks, np.int32)
+    cs = np.ascontiguousarray(chunk_slot, np.int32)
+    bh = np.ascontiguousarray(block_hash, np.uint64)
+    bo = np.ascontiguousarray(blk_off, np.int64)
+    co = np.ascontiguousarray(chunk_off, np.int64)
+    fs = np.ascontiguousarray(free_slots, np.int32)
+    rq = np.ascontiguousarray(np.broadcast_to(np.asarray(requested).astype(bool), (R,)), np.uint8)
+    dec = np.ascontiguousarray(decisions, np.int32)
+    retr = np.zeros((max(nchunks, 1), 4), np.int32)
+    ordn = np.zeros((max(nchunks, 1), 4), np.int32)
+    store = np.zeros((max(nchunks, 1), 4), np.int32)
+    keys = np.zeros(max(nchunks, 1), np.uint64)
+    nr, no, ns, nd = _i32(0), _i32(0), _i32(0), _i32(0)
+    rc = host_lib().kv_build_jobs_routed(hit.ctypes.data, cs.ctypes.data, bh.ctypes.data, bo.ctypes.data,
+                                         co.ctypes.data, R, blocks_per_chunk, fs.ctypes.data if fs.size else None,
+                                         fs.size, rq.ctypes.data, dec.ctypes.data, retr.ctypes.data, ct.byref(nr),
+                                         ordn.ctypes.data, ct.byref(no), store.ctypes.data, keys.ctypes.data,
+                                         ct.byref(ns), ct.byref(nd))
+    if rc < 0 and rc != KV_ENOSPC:
+        raise KvError(rc, "kv_build_jobs_routed")
+    return (retr[:nr.value].copy(), ordn[:no.value].copy(), store[:ns.value].copy(), keys[:ns.value].copy(),
+            nd.value, rc)
+
+
+def kv_ttr_static(objs, obj_bytes, resident, static_rate: float) -> float:
+    """Static TTR of a claim over its distinct objects `objs` (ids into obj_bytes / resident)."""
+    o = np.ascontiguousarray(objs, np.int32).reshape(-1)
+    b = np.ascontiguousarray(obj_bytes, np.float64).reshape(-1)
+    r = np.ascontiguousarray(np.asarray(resident).astype(bool), np.uint8).reshape(-1)
+    if r.size != b.size:
+        raise ValueError("resident must hold one flag per object")
+    out = _dbl(0.0)
+    _check(host_lib().kv_ttr_static(o.size, o.ctypes.data, b.size, b.ctypes.data, r.ctypes.data, float(static_rate),
+                                    ct.byref(out)), "kv_ttr_static")
+    return out.value
+
+
+def kv_ttr_state_aware(objs, obj_bytes, resident, queued, ready_at, now_s: float, busy_until_s: float,
+                       stage_rate: float) -> float:
+    """State-aware TTR of a claim against the staging queue's state."""
+    o = np.ascontiguousarray(objs, np.int32).reshape(-1)
+    b = np.ascontiguousarray(obj_bytes, np.float64).reshape(-1)
+    r = np.ascontiguousarray(np.asarray(resident).astype(bool), np.uint8).reshape(-1)
+    q = np.ascontiguousarray(np.asarray(queued).astype(bool), np.uint8).reshape(-1)
+    t = np.ascontiguousarray(ready_at, np.float64).reshape(-1)
+    if not (r.size == q.size == t.size == b.size):
+        raise ValueError("per-object arrays must have the same length")
+    out = _dbl(0.0)
+    _check(host_lib().kv_ttr_state_aware(o.size, o.ctypes.data, b.size, b.ctypes.data, r.ctypes.data,
+                                         q.ctypes.data, t.ctypes.data, float(now_s), float(busy_until_s),
+                                         float(stage_rate), ct.byref(out)), "kv_ttr_state_aware")
+    return out.value
 
 
 def _layer_array(layers: Sequence) -> ct.Array:
@@ -339,7 +461,7 @@ def kv_retrieve_scatter(layout: KvLayout, d_staging, layers: Sequence, d_block_t
 def kv_retrieve_plan(layout: KvLayout, h_jobs: np.ndarray) -> int:
     """The retrieve variant (KV_RETRIEVE_*) for a job list ([n,4] int32, grouped by slot)."""
     hj = np.ascontiguousarray(h_jobs, np.int32).reshape(-1, 4)
-    return _check(lib().kv_retrieve_plan(ct.byref(layout), hj.ctypes.data if hj.size else None, hj.shape[0]),
+    return _check(host_lib().kv_retrieve_plan(ct.byref(layout), hj.ctypes.data if hj.size else None, hj.shape[0]),
                   "kv_retrieve_plan")
 
 
@@ -446,7 +568,7 @@ def kv_retrieve_pipelined(pipeline: KvPipeline, layout: KvLayout, h_lower_tier, 
 def kv_group_jobs_by_slot(jobs: np.ndarray) -> np.ndarray:
     """Returns the jobs ([n,4] int32) stably ordered by slot (a copy)."""
     jb = np.ascontiguousarray(jobs, np.int32).reshape(-1, 4).copy()
-    _check(lib().kv_group_jobs_by_slot(jb.ctypes.data if jb.size else None, jb.shape[0]), "kv_group_jobs_by_slot")
+    _check(host_lib().kv_group_jobs_by_slot(jb.ctypes.data if jb.size else None, jb.shape[0]), "kv_group_jobs_by_slot")
     return jb
 
 
@@ -454,7 +576,7 @@ def kv_validate_jobs(layout: KvLayout, block_tables: np.ndarray, jobs: np.ndarra
     """Returns KV_OK, KV_ERANGE or KV_EDUP (other errors raise)."""
     bt = np.ascontiguousarray(block_tables, np.int32)
     jb = np.ascontiguousarray(jobs, np.int32).reshape(-1, 4)
-    rc = lib().kv_validate_jobs(ct.byref(layout), bt.ctypes.data, bt.shape[1], bt.shape[0], jb.ctypes.data,
+    rc = host_lib().kv_validate_jobs(ct.byref(layout), bt.ctypes.data, bt.shape[1], bt.shape[0], jb.ctypes.data,
                                 jb.shape[0], 1 if is_store else 0)
     if rc not in (KV_OK, KV_ERANGE, KV_EDUP):
         raise KvError(rc, "kv_validate_jobs")
@@ -464,7 +586,7 @@ def kv_validate_jobs(layout: KvLayout, block_tables: np.ndarray, jobs: np.ndarra
 def kv_commit_should_stage(ttu_s: float, ttr_s: float, free_protected_bytes: int, claim_new_bytes: int,
                            claim_total_bytes: int, budget_bytes: int, retrieval_requested: bool) -> int:
     """Returns a KV_DEFER/KV_COMMIT/KV_BLOCKED/KV_ORDINARY decision or KV_EINVAL."""
-    return lib().kv_commit_should_stage(ttu_s, ttr_s, free_protected_bytes, claim_new_bytes, claim_total_bytes,
+    return host_lib().kv_commit_should_stage(ttu_s, ttr_s, free_protected_bytes, claim_new_bytes, claim_total_bytes,
                                         budget_bytes, 1 if retrieval_requested else 0)
 
 
@@ -482,7 +604,7 @@ def kv_commit_should_stage_n(ttu, ttr, free_protected_bytes: int, claim_new, cla
         raise ValueError("all claim arrays must have the same length")
     out = np.zeros(n, np.int32)
     if n:
-        _check(lib().kv_commit_should_stage_n(n, a.ctypes.data, b.ctypes.data, int(free_protected_bytes),
+        _check(host_lib().kv_commit_should_stage_n(n, a.ctypes.data, b.ctypes.data, int(free_protected_bytes),
                                               cn.ctypes.data, ct_.ctypes.data, int(budget_bytes), rq.ctypes.data,
                                               out.ctypes.data), "kv_commit_should_stage_n")
     return out
@@ -515,7 +637,7 @@ def kv_sim_run(config: KvSimConfig, obj_bytes, arrival, manifests, uncached, out
     if trace:
         cap = 64 * (N + ob.size) + 1024
         buf = (KvSimEvent * cap)()
-    rc = lib().kv_sim_run(ct.byref(config), ob.ctypes.data if ob.size else None, ob.size, arr.ctypes.data,
+    rc = host_lib().kv_sim_run(ct.byref(config), ob.ctypes.data if ob.size else None, ob.size, arr.ctypes.data,
                           off.ctypes.data, objs.ctypes.data, unc.ctypes.data, out.ctypes.data, N, ft.ctypes.data,
                           dn.ctypes.data, ct.byref(res), ct.cast(buf, ct.c_void_p) if buf is not None else None,
                           cap, ct.byref(n_tr))

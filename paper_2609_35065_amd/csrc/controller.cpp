@@ -43,6 +43,39 @@
 
 namespace {
 
+// TTR estimators (Section 3.1, "Storage-estimated time-to-ready") over a
+// claim's distinct KV objects; shared by the simulator and the C ABI.
+// Static: the non-resident bytes over a fixed rate, the claim in isolation.
+template <class Flag>
+double ttr_static_of(const int32_t *objs, size_t n, const double *bytes, const Flag *resident, double rate) {
+    double s = 0.0;
+    for (size_t k = 0; k < n; ++k)
+        if (!resident[objs[k]]) s += bytes[objs[k]];
+    return s / rate;
+}
+
+// State-aware: the staging queue projected from `now`.  An object already
+// queued keeps its completion time; a non-resident object not yet queued is
+// appended behind the queue's tail (busy until `busy_until`) at the staging
+// rate; the last object to become resident decides.
+template <class Flag>
+double ttr_state_of(const int32_t *objs, size_t n, const double *bytes, const Flag *resident, const Flag *queued,
+                    const double *ready_at, double now, double busy_until, double stage_rate) {
+    double t_end = now;
+    double tail = std::max(busy_until, now);
+    for (size_t k = 0; k < n; ++k) {
+        const int32_t o = objs[k];
+        if (resident[o]) continue;
+        if (queued[o]) {
+            t_end = std::max(t_end, ready_at[o]);
+        } else {
+            tail = tail + bytes[o] / stage_rate;
+            t_end = std::max(t_end, tail);
+        }
+    }
+    return t_end - now;
+}
+
 enum { PLANNED, STAGING, STAGEREADY, TRANSFERRING, RELEASED, ORDINARY };
 enum { EV_ARRIVAL, EV_OBJ_READY, EV_FETCH_END, EV_TRANSFER_END, EV_REQ_END, EV_TICK };
 enum { PH_WAIT, PH_FETCH, PH_RUN };
@@ -214,25 +247,12 @@ class Sim {
     }
 
     double ttr_static(int32_t i) const {
-        double s = 0.0;
-        for (int32_t o : uniq_[i])
-            if (!resident_[o]) s += bytes_[o];
-        return s / c_.static_rate;
+        return ttr_static_of(uniq_[i].data(), uniq_[i].size(), bytes_.data(), resident_.data(), c_.static_rate);
     }
 
     double ttr_state(int32_t i) const {
-        double t_end = now_;
-        double tail = std::max(busy_until_, now_);
-        for (int32_t o : uniq_[i]) {
-            if (resident_[o]) continue;
-            if (queued_[o]) {
-                t_end = std::max(t_end, ready_at_[o]);
-            } else {
-                tail = tail + bytes_[o] / c_.stage_rate;
-                t_end = std::max(t_end, tail);
-            }
-        }
-        return t_end - now_;
+        return ttr_state_of(uniq_[i].data(), uniq_[i].size(), bytes_.data(), resident_.data(), queued_.data(),
+                            ready_at_.data(), now_, busy_until_, c_.stage_rate);
     }
 
     double projected_end(int32_t i) const {
@@ -422,5 +442,39 @@ extern "C" int kv_sim_run(const kv_sim_config *cfg, const double *h_obj_bytes, i
         h_done[i] = sim.done()[i];
     }
     if (trace_len) *trace_len = sim.trace_len();
+    return KV_OK;
+}
+
+namespace {
+
+// Objects of a claim: non-negative ids below num_objects.
+bool objs_ok(int32_t n, const int32_t *objs, int32_t num_objects) {
+    for (int32_t k = 0; k < n; ++k)
+        if (objs[k] < 0 || objs[k] >= num_objects) return false;
+    return true;
+}
+
+}  // namespace
+
+extern "C" int kv_ttr_static(int32_t num_objs, const int32_t *h_objs, int32_t num_objects, const double *h_obj_bytes,
+                             const uint8_t *h_resident, double static_rate, double *ttr_s) {
+    if (num_objs < 0 || num_objects < 0 || !ttr_s || !(static_rate > 0)) return KV_EINVAL;
+    if (num_objs > 0 && (!h_objs || !h_obj_bytes || !h_resident || !objs_ok(num_objs, h_objs, num_objects)))
+        return KV_EINVAL;
+    *ttr_s = ttr_static_of(h_objs, (size_t)num_objs, h_obj_bytes, h_resident, static_rate);
+    return KV_OK;
+}
+
+extern "C" int kv_ttr_state_aware(int32_t num_objs, const int32_t *h_objs, int32_t num_objects,
+                                  const double *h_obj_bytes, const uint8_t *h_resident, const uint8_t *h_queued,
+                                  const double *h_ready_at, double now_s, double busy_until_s, double stage_rate,
+                                  double *ttr_s) {
+    if (num_objs < 0 || num_objects < 0 || !ttr_s || !(stage_rate > 0) || isnan(now_s) || isnan(busy_until_s))
+        return KV_EINVAL;
+    if (num_objs > 0 && (!h_objs || !h_obj_bytes || !h_resident || !h_queued || !h_ready_at ||
+                         !objs_ok(num_objs, h_objs, num_objects)))
+        return KV_EINVAL;
+    *ttr_s = ttr_state_of(h_objs, (size_t)num_objs, h_obj_bytes, h_resident, h_queued, h_ready_at, now_s,
+                          busy_until_s, stage_rate);
     return KV_OK;
 }

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "host.h"
 #include "tempokv.h"
 
 namespace tkv {
@@ -65,9 +66,8 @@ hipError_t launch_lookup(const IndexEntry *table, int log2cap, const uint64_t *b
                          const int64_t *blk_off, int32_t num_reqs, int32_t bpc, const int64_t *chunk_off,
                          int32_t *chunk_slot, int32_t *hit_chunks, hipStream_t stream);
 
-// Argument checks and launch parameters shared by the copy entry points
-// (api.hip).  Return KV_OK or a negative kv_status.
-int check_layout(const kv_layout *lo);
+// Launch parameters shared by the copy entry points (api.hip), after every
+// argument check.  Returns KV_OK or a negative kv_status.
 int make_copy_params(CopyParams &p, const kv_layout *lo, const void *staging, const void *const *layers,
                      const int32_t *bt, int32_t bt_stride, int32_t num_reqs, const kv_job *jobs, int32_t num_jobs);
 

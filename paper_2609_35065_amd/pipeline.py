@@ -1,8 +1,9 @@
 """One pass of the staging hot path over a batch of requests, on one GPU.
 
 A pass is:  hash (kv_hash_prefix) -> lookup (kv_lookup) -> one device-to-host
-copy of the lookup result -> host job build (kv_build_jobs) and commitment
-decisions (kv_commit_should_stage_n) -> one host-to-device copy of the jobs ->
+copy of the lookup result -> commitment decisions for the requests' claims
+(kv_decide_claims) and the host job build that routes each claim by its
+decision (kv_build_jobs_routed) -> one host-to-device copy of the jobs ->
 retrieve scatter (kv_retrieve_plan picks the copy variant, or the variant
 tune_retrieve found faster for that plan on this path's pool;
 kv_retrieve_scatter_as runs it) -> store gather (kv_store_gather) ->
@@ -22,6 +23,26 @@ picks how the retrieve reaches them:
 In the two staged modes the store gathers into the HBM staging buffer and
 copies the stored slots back to host memory (kv_stage_out).
 
+Commitment (Section 3.2).  Each request's claim is its matched prefix.  A
+pass takes, per request, whether retrieval is requested now (the request
+runs in this pass), its TTU and TTR estimates, and a protected-capacity
+budget (``ClaimInputs``; by default every request runs, TTU = TTR = 0, and the
+budget is the whole staging buffer, so every claim commits).  The decisions
+route the work:
+  KV_COMMIT, requested      the claim's chunks take the protected route: the
+                            scatter from the HBM fast tier (staged modes: DMA
+                            into HBM first, then the gated scatter);
+  KV_ORDINARY               the ordinary retrieval path: the chunks are read
+                            where they lie without protection (staged modes:
+                            zero-copy from the lower tier, nothing is staged
+                            into HBM for them), in a launch of their own;
+  KV_COMMIT, not requested  staging begins at commitment: in staged modes the
+                            claim's chunks not yet in HBM are copied there;
+  KV_BLOCKED, KV_DEFER      the claim stays PLANNED; its request gets no jobs.
+Only requests whose retrieval is requested get retrieve or store jobs.
+Protection lasts until the pass's retrieval completes, so each pass starts
+with nothing protected.
+
 This module only sequences the C calls and owns the buffers they read and
 write; it computes nothing itself.
 """
@@ -33,23 +54,40 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (KV_COMMIT, KV_ENOSPC, KV_RETRIEVE_QUAD, KV_RETRIEVE_STREAM, RETRIEVE_KIND_NAMES, KvIndex, KvLayout,
-               KvPipeline, kv_build_jobs, kv_commit_should_stage_n,
+from . import (KV_COMMIT, KV_ORDINARY, KV_RETRIEVE_QUAD, KV_RETRIEVE_STREAM, RETRIEVE_KIND_NAMES, KvIndex,
+               KvLayout, KvPipeline, kv_build_jobs_routed, kv_chunk_keys, kv_decide_claims,
                kv_group_jobs_by_slot, kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_pipelined,
-               kv_retrieve_plan, kv_retrieve_scatter_as, kv_stage_out, kv_store_gather, make_layout)
+               kv_retrieve_plan, kv_retrieve_scatter_as, kv_stage_in, kv_stage_out, kv_store_gather, make_layout)
 
 LOWER_TIER_MODES = ("zero-copy", "pipelined", "serialized")
 
 
 @dataclass
+class ClaimInputs:
+    """Per-request inputs of a pass's commitment decisions (Section 3.2)."""
+    requested: np.ndarray        # bool [R]: retrieval requested now (the request runs in this pass)
+    ttu: np.ndarray              # float64 [R], seconds until retrieval would begin
+    ttr: np.ndarray              # float64 [R], seconds until the claim would be stage-ready
+    budget_bytes: int            # protected-capacity budget
+
+    @staticmethod
+    def all_now(num_reqs: int, budget_bytes: int) -> "ClaimInputs":
+        """Every request runs now (retrieval requested, TTU = TTR = 0)."""
+        return ClaimInputs(np.ones(num_reqs, bool), np.zeros(num_reqs), np.zeros(num_reqs), int(budget_bytes))
+
+
+@dataclass
 class PassStats:
-    num_retrieve: int = 0
+    num_retrieve: int = 0        # jobs on the protected route
+    num_ordinary: int = 0        # jobs on the ordinary route
     num_store: int = 0
     dropped: int = 0
-    retrieve_bytes: int = 0      # payload copied by the scatter (read = written)
+    retrieve_bytes: int = 0      # payload copied by the scatter, both routes (read = written)
+    ordinary_bytes: int = 0      # of which on the ordinary route
     store_bytes: int = 0
     staged_bytes: int = 0        # lower tier -> HBM by DMA (staged modes)
     commits: int = 0
+    reserved_bytes: int = 0      # protected bytes reserved by the pass's commitments
     decisions: Dict[int, int] = field(default_factory=dict)
 
 
@@ -89,6 +127,7 @@ class StagingPath:
             if w.staging_in_host:
                 self.staging_host = torch.empty(w.staged_bytes(), dtype=torch.uint8, pin_memory=True)
                 self.staging_ptr = kv_host_device_pointer(self.staging_host.data_ptr())
+                self.host_mapped_ptr = self.staging_ptr     # the lower tier read in place (ordinary route)
                 self.staging = None
                 if self.staged_mode:
                     self.staging = torch.empty(w.staged_bytes(), dtype=torch.uint8, device=d)
@@ -106,7 +145,9 @@ class StagingPath:
         self.last_store_keys = np.zeros(0, np.uint64)
         self.last_store_slots = np.zeros(0, np.int32)
         self.last_retrieve = np.zeros((0, 4), np.int32)
+        self.last_ordinary = np.zeros((0, 4), np.int32)
         self.last_store = np.zeros((0, 4), np.int32)
+        self.last_decisions = np.zeros(0, np.int32)
         self.retrieve_kind: Optional[int] = None
         # planned retrieve variant -> variant to run instead (set by tune_retrieve)
         self.retrieve_choice: Dict[int, int] = {}
@@ -203,21 +244,28 @@ class StagingPath:
                 dh = torch.empty(max(int(boff[-1]), 1), dtype=torch.int64, device=self.dev)
                 kv_hash_prefix(dt, doff, off.size - 1, self.hash_seed, dboff, dh, self.stream)
                 h = dh.cpu().numpy().view(np.uint64)
-            keys = np.array([h[boff[p] + (j + 1) * self.bpc - 1] for p, j in w.prestage_chunks], np.uint64)
+            nc = np.diff(boff) // self.bpc
+            coff = np.zeros(off.size, np.int64)
+            np.cumsum(nc, out=coff[1:])
+            ck = kv_chunk_keys(h, boff, self.bpc, coff)
+            keys = np.array([ck[coff[p] + j] for p, j in w.prestage_chunks], np.uint64)
             self.index.insert(keys, np.arange(P, dtype=np.int32), self.lookup_stream)
         self.free = list(range(P, w.num_slots))
         self.stream.synchronize()
         self.lookup_stream.synchronize()
 
     # ------------------------------------------------------------------
-    def run_pass(self, evict_stored: bool = False, validate: bool = False, timers: Optional[dict] = None) -> PassStats:
+    def run_pass(self, evict_stored: bool = False, validate: bool = False, timers: Optional[dict] = None,
+                 claims: Optional[ClaimInputs] = None) -> PassStats:
         """One pass of the hot path over the current batch.
 
         ``timers``: optional dict; when given, a (start, end) pair of
-        torch.cuda.Event is appended under "hash", "lookup", "retrieve" and
-        "store" around each launch, recorded on the stream it runs on."""
+        torch.cuda.Event is appended under "hash", "lookup", "retrieve",
+        "ordinary" and "store" around each launch, recorded on the stream it
+        runs on.  ``claims``: the commitment inputs (default: every request
+        runs now and the budget is the whole staging buffer)."""
         self.launch_lookup(timers)
-        return self.complete_pass(evict_stored, validate, timers)
+        return self.complete_pass(evict_stored, validate, timers, claims)
 
     def launch_lookup(self, timers: Optional[dict] = None) -> None:
         """Enqueue the first half of a pass on the lookup stream: hash, lookup
@@ -240,11 +288,14 @@ class StagingPath:
             self.h_hit.copy_(self.hit, non_blocking=True)
             self._lookup_done.record(ls)
 
+    def default_claims(self) -> ClaimInputs:
+        return ClaimInputs.all_now(self.batch.num_reqs, self.w.num_slots * self.w.shape.slot_bytes)
+
     def complete_pass(self, evict_stored: bool = False, validate: bool = False,
-                      timers: Optional[dict] = None) -> PassStats:
-        """Second half of a pass: wait for the lookup results, build the jobs
-        and decisions on the host, enqueue the copies on this path's stream
-        and the index update on the lookup stream."""
+                      timers: Optional[dict] = None, claims: Optional[ClaimInputs] = None) -> PassStats:
+        """Second half of a pass: wait for the lookup results, decide the
+        claims and build the jobs on the host, enqueue the copies on this
+        path's stream and the index update on the lookup stream."""
         w = self.batch
         R = w.num_reqs
         st = PassStats()
@@ -254,28 +305,26 @@ class StagingPath:
         cs = self.h_chunk_slot.numpy()[:nch]
         hit = self.h_hit.numpy()[:R]
         free = np.array(self.free, np.int32)
-        retr, store, skeys, dropped, rc = kv_build_jobs(hit, cs, bh, self.blk_off_h, self.chunk_off_h, self.bpc, free)
-        st.num_retrieve, st.num_store, st.dropped = len(retr), len(store), dropped
         slot_bytes = w.shape.slot_bytes
-        st.retrieve_bytes = len(retr) * slot_bytes
+        cl = claims if claims is not None else self.default_claims()
+        dec, protected, reserved = kv_decide_claims(hit, cs, self.chunk_off_h, cl.ttu, cl.ttr, cl.requested,
+                                                    slot_bytes, cl.budget_bytes, w.num_slots)
+        retr, ordn, store, skeys, dropped, rc = kv_build_jobs_routed(hit, cs, bh, self.blk_off_h, self.chunk_off_h,
+                                                                     self.bpc, free, cl.requested, dec)
+        st.num_retrieve, st.num_ordinary, st.num_store, st.dropped = len(retr), len(ordn), len(store), dropped
+        st.retrieve_bytes = (len(retr) + len(ordn)) * slot_bytes
+        st.ordinary_bytes = len(ordn) * slot_bytes
         st.store_bytes = len(store) * slot_bytes
-        # commitment decision per request claim: retrieval is requested now;
-        # the claim's matched footprint must fit the staged capacity
-        budget = self.w.num_slots * slot_bytes
-        claims = np.nonzero(hit > 0)[0]
-        if claims.size:
-            total = hit[claims].astype(np.uint64) * np.uint64(slot_bytes)
-            dec = kv_commit_should_stage_n(np.zeros(claims.size), np.zeros(claims.size), budget,
-                                           np.zeros(claims.size, np.uint64), total, budget,
-                                           np.ones(claims.size, bool))
-            for d, c in zip(*np.unique(dec, return_counts=True)):
-                st.decisions[int(d)] = int(c)
-            st.commits = int(np.count_nonzero(dec == KV_COMMIT))
+        st.reserved_bytes = reserved
+        for d, c in zip(*np.unique(dec, return_counts=True)):
+            st.decisions[int(d)] = int(c)
+        st.commits = int(np.count_nonzero(dec == KV_COMMIT))
         if validate:
             from . import kv_validate_jobs
-            assert kv_validate_jobs(self.layout, w.block_tables, retr, False) == 0 or len(retr) == 0
+            both = np.concatenate([retr, ordn])
+            assert kv_validate_jobs(self.layout, w.block_tables, both, False) == 0 or len(both) == 0
             assert kv_validate_jobs(self.layout, w.block_tables, store, True) == 0 or len(store) == 0
-        nr, ns = len(retr), len(store)
+        nr, no, ns = len(retr), len(ordn), len(store)
         nres = nr   # jobs whose chunk is already in the staging buffer the scatter reads
         par = self._parity
         self._parity ^= 1
@@ -291,7 +340,11 @@ class StagingPath:
                     grouped = np.concatenate([grouped[here], grouped[~here]])
                     nres = int(here.sum())
                 self.h_retr.numpy()[:nr] = grouped
-                self.d_retr[:nr].copy_(self.h_retr[:nr], non_blocking=True)
+            if no:
+                # the ordinary route's jobs follow the protected route's in the same upload
+                self.h_retr.numpy()[nr:nr + no] = kv_group_jobs_by_slot(ordn)
+            if nr + no:
+                self.d_retr[:nr + no].copy_(self.h_retr[:nr + no], non_blocking=True)
             if ns:
                 self.h_store.numpy()[:ns] = store
                 self.d_store[:ns].copy_(self.h_store[:ns], non_blocking=True)
@@ -317,6 +370,25 @@ class StagingPath:
                 self.resident[staged] = True
                 st.staged_bytes = int(staged.size) * slot_bytes
             self._ev_end(e)
+            if no:
+                # ordinary retrieval: read in place, unprotected (from the lower tier when there is one)
+                e = self._ev(timers, "ordinary")
+                src = self.host_mapped_ptr if self.staged_mode else self.staging_ptr
+                okind = kv_retrieve_plan(self.layout, self.h_retr.numpy()[nr:nr + no])
+                kv_retrieve_scatter_as(okind, self.layout, src, self.layers, self.bt, w.bt_stride, R,
+                                       self.d_retr[nr:nr + no], no, self.stream)
+                self._ev_end(e)
+            if self.staged_mode:
+                # staging begins at commitment for claims whose retrieval is not requested yet
+                ahead = np.nonzero((protected != 0) & ~self.resident)[0].astype(np.int32)
+                if ahead.size:
+                    if self.copy_stream is not self.stream:
+                        self.copy_stream.wait_stream(self.stream)
+                    kv_stage_in(self.layout, self.staging_host, self.staging, ahead, self.copy_stream)
+                    # later scatters read these slots as resident: they wait for the copies
+                    self.stream.wait_stream(self.copy_stream)
+                    self.resident[ahead] = True
+                    st.staged_bytes += int(ahead.size) * slot_bytes
             e = self._ev(timers, "store")
             kv_store_gather(self.layout, self.staging_ptr, self.layers, self.bt, w.bt_stride, R, self.d_store, ns,
                             self.stream)
@@ -330,7 +402,8 @@ class StagingPath:
         used = set(int(x) for x in store[:, 0])
         self.free = [s for s in self.free if s not in used]
         self.last_store_keys, self.last_store_slots = skeys, store[:, 0].copy()
-        self.last_retrieve, self.last_store = retr, store
+        self.last_retrieve, self.last_ordinary, self.last_store = retr, ordn, store
+        self.last_decisions = dec
         if evict_stored and ns:
             self.evict_last()
         return st

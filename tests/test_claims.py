@@ -1,0 +1,276 @@
+"""Commitment decisions over a batch of claims, the routed job build, and the
+two TTR estimators.
+
+The oracle's decisions (oracle/pipeline.py, OraclePath.decide_claims) are
+pinned to what Section 3.2 fixes: requested claims are considered before the
+others, a claim that cannot commit does not hold up later ones, shared objects
+are reserved once, a protected commitment needs the full footprint within the
+budget, and an unprotectable requested claim takes the ordinary path.  The
+library's kv_decide_claims and kv_build_jobs_routed must then agree with the
+oracle on random batches, and kv_ttr_static / kv_ttr_state_aware with the
+controller oracle's estimators, which are pinned to closed forms here."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2609_35065_amd as kv
+import workloads as W
+from oracle import controller as ctl
+from oracle.pipeline import OraclePath
+
+SHAPE = W.KVShape(2, 2, 64, 2, 16, 64)          # slot_bytes = 64 KiB
+SB = SHAPE.slot_bytes
+
+
+class Claims:
+    def __init__(self, requested, ttu, ttr, budget_bytes):
+        self.requested = np.asarray(requested, bool)
+        n = self.requested.size
+        self.ttu = np.broadcast_to(np.asarray(ttu, np.float64), (n,)).copy()
+        self.ttr = np.broadcast_to(np.asarray(ttr, np.float64), (n,)).copy()
+        self.budget_bytes = int(budget_bytes)
+
+
+def _oracle_path(num_reqs, seed=3):
+    w = W.small_random(seed, SHAPE, num_reqs=num_reqs, max_len=512)
+    return OraclePath(w, with_kv=False), w
+
+
+def _claims_layout(o, hits, slots):
+    """hit counts and a chunk_slot array in the workload's chunk layout."""
+    co = o.chunk_off
+    cs = np.full(int(co[-1]), -1, np.int32)
+    hit = np.zeros(len(hits), np.int32)
+    for r, (h, ss) in enumerate(zip(hits, slots)):
+        nc = int(co[r + 1] - co[r])
+        h = min(h, nc)
+        hit[r] = h
+        cs[co[r]:co[r] + h] = ss[:h]
+    return hit, cs
+
+
+# ---------------------------------------------------------------------------
+# pins of the oracle's decisions (Section 3.2)
+# ---------------------------------------------------------------------------
+
+def _four_request_path():
+    # four requests of 512 tokens (8 chunks of 64 tokens each)
+    w = W._assemble("claims-4x512", SHAPE, 5, [512] * 4, [0, 0, 1, 1], [256] * 4, 2,
+                    prestage=[(p, j) for p in range(2) for j in range(4)], num_slots=16, pool_factor=1.25)
+    return OraclePath(w, with_kv=False)
+
+
+def test_oracle_everything_fits_commits():
+    o = _four_request_path()
+    hit, cs = _claims_layout(o, [2, 2, 2, 2], [[0, 1], [0, 1], [4, 5], [4, 5]])
+    d = o.decide_claims(hit, cs, Claims([1, 1, 1, 1], 0, 0, 100 * SB))
+    assert d == [oracle.COMMIT] * 4
+
+
+def test_oracle_shared_objects_reserved_once():
+    # budget of two objects; all four claims name the same two: each after the first needs no free capacity
+    o = _four_request_path()
+    hit, cs = _claims_layout(o, [2, 2, 2, 2], [[0, 1]] * 4)
+    d = o.decide_claims(hit, cs, Claims([1, 1, 1, 1], 0, 0, 2 * SB))
+    assert d == [oracle.COMMIT] * 4
+
+
+def test_oracle_requested_claims_go_first():
+    # request 0 is only eligible by timing, request 1 has its retrieval requested; one fits
+    o = _four_request_path()
+    hit, cs = _claims_layout(o, [2, 2, 0, 0], [[0, 1], [4, 5], [], []])
+    d = o.decide_claims(hit, cs, Claims([0, 1, 1, 1], [-1.0, 0, 0, 0], [0.0, 0, 0, 0], 2 * SB))
+    assert d[1] == oracle.COMMIT and d[0] == oracle.BLOCKED
+
+
+def test_oracle_blocked_claim_does_not_hold_up_later_ones():
+    # claim 0 needs 3 objects with room for 2; claim 1 needs 1 and still commits
+    o = _four_request_path()
+    hit, cs = _claims_layout(o, [3, 1, 0, 0], [[0, 1, 2], [4], [], []])
+    d = o.decide_claims(hit, cs, Claims([0, 0, 0, 0], [0.0] * 4, [1.0] * 4, 2 * SB))
+    assert d[0] == oracle.BLOCKED and d[1] == oracle.COMMIT
+
+
+def test_oracle_unprotectable_requested_claim_takes_ordinary_path():
+    o = _four_request_path()
+    hit, cs = _claims_layout(o, [2, 2, 0, 0], [[0, 1], [4, 5], [], []])
+    d = o.decide_claims(hit, cs, Claims([1, 1, 1, 1], 0, 0, 3 * SB))
+    assert d[:2] == [oracle.COMMIT, oracle.ORDINARY]
+
+
+def test_oracle_full_footprint_must_fit_budget():
+    # claim 1's objects are all protected by claim 0, but its footprint (3) exceeds the budget (2)
+    o = _four_request_path()
+    hit, cs = _claims_layout(o, [2, 3, 0, 0], [[0, 1], [0, 1, 2], [], []])
+    d = o.decide_claims(hit, cs, Claims([1, 1, 1, 1], 0, 0, 2 * SB))
+    assert d[:2] == [oracle.COMMIT, oracle.ORDINARY]
+
+
+def test_oracle_positive_laxity_defers():
+    o = _four_request_path()
+    hit, cs = _claims_layout(o, [2, 2, 0, 0], [[0, 1], [4, 5], [], []])
+    d = o.decide_claims(hit, cs, Claims([0, 0, 0, 0], [2.0, 0.5, 0, 0], [1.0, 0.5, 0, 0], 100 * SB))
+    assert d[0] == oracle.DEFER and d[1] == oracle.COMMIT
+
+
+def test_oracle_reservations_accumulate():
+    # three disjoint claims of one object each against a budget of two: the third finds no free capacity
+    o = _four_request_path()
+    hit, cs = _claims_layout(o, [1, 1, 1, 0], [[0], [4], [1], []])
+    d = o.decide_claims(hit, cs, Claims([1, 1, 1, 1], 0, 0, 2 * SB))
+    assert d[:3] == [oracle.COMMIT, oracle.COMMIT, oracle.ORDINARY]
+
+
+# ---------------------------------------------------------------------------
+# the library against the oracle
+# ---------------------------------------------------------------------------
+
+def _random_case(rng, o):
+    R = o.batch.num_reqs
+    co = o.chunk_off
+    nslot = o.batch.num_slots
+    hits, slots = [], []
+    for r in range(R):
+        nc = int(co[r + 1] - co[r])
+        h = int(rng.integers(0, nc + 1))
+        # objects drawn from a small pool so that claims share them
+        pool = rng.permutation(min(nslot, 12))[:max(h, 1)]
+        hits.append(h)
+        slots.append([int(x) for x in pool[:h]])
+    hit, cs = _claims_layout(o, hits, slots)
+    # the chunks after the hit prefix: some present (a key after a miss), most missing
+    for r in range(R):
+        for j in range(int(hit[r]) + 1, int(co[r + 1] - co[r])):
+            if rng.random() < 0.2:
+                cs[co[r] + j] = int(rng.integers(0, nslot))
+    requested = rng.random(R) < 0.6
+    ttu = rng.choice([-1.0, 0.0, 0.5, 2.0, math.inf], R)
+    ttr = rng.choice([0.0, 0.5, 1.0, math.inf], R)
+    budget = int(rng.integers(0, 8)) * SB + int(rng.integers(0, 2)) * (SB // 2)
+    return hit, cs, Claims(requested, ttu, ttr, budget)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_decide_claims_matches_oracle(seed):
+    rng = np.random.default_rng(seed)
+    o, w = _oracle_path(int(rng.integers(1, 14)), seed=seed + 100)
+    hit, cs, cl = _random_case(rng, o)
+    want = o.decide_claims(hit, cs, cl)
+    got, prot, reserved = kv.kv_decide_claims(hit, cs, o.chunk_off, cl.ttu, cl.ttr, cl.requested, SB,
+                                              cl.budget_bytes, w.num_slots)
+    assert got.tolist() == want
+    # the ledger: exactly the objects of committed claims, each counted once
+    objs = sorted({int(cs[o.chunk_off[r] + j]) for r in range(len(want)) if want[r] == oracle.COMMIT
+                   for j in range(int(hit[r]))})
+    assert np.nonzero(prot)[0].tolist() == objs
+    assert reserved == len(objs) * SB
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_build_jobs_routed_matches_oracle(seed):
+    rng = np.random.default_rng(1000 + seed)
+    o, w = _oracle_path(int(rng.integers(1, 14)), seed=seed + 300)
+    hit, cs, cl = _random_case(rng, o)
+    # requested claims all decided COMMIT or ORDINARY (the only outcomes when retrieval is requested)
+    dec = np.array(o.decide_claims(hit, cs, cl), np.int32)
+    bh = np.arange(1, int(o.blk_off[-1]) + 1, dtype=np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+    o.free = [int(s) for s in rng.permutation(w.num_slots)[:int(rng.integers(0, w.num_slots + 1))]]
+    retr, store, skeys, dropped = o._running_jobs(bh, cs, hit, cl.requested)
+    ordinary = np.array([dec[q[1]] == oracle.ORDINARY for q in retr], bool)
+    want_r = retr[~ordinary] if len(retr) else retr
+    want_o = retr[ordinary] if len(retr) else retr
+    r2, o2, s2, k2, d2, rc = kv.kv_build_jobs_routed(hit, cs, bh, o.blk_off, o.chunk_off, o.bpc,
+                                                     np.array(o.free, np.int32), cl.requested, dec)
+    assert np.array_equal(r2.reshape(-1, 4), np.asarray(want_r).reshape(-1, 4))
+    assert np.array_equal(o2.reshape(-1, 4), np.asarray(want_o).reshape(-1, 4))
+    assert np.array_equal(s2.reshape(-1, 4), np.asarray(store).reshape(-1, 4))
+    assert np.array_equal(k2, skeys) and d2 == dropped
+    assert (rc == kv.KV_ENOSPC) == (dropped > 0)
+
+
+def test_build_jobs_routed_equals_build_jobs_when_all_commit():
+    rng = np.random.default_rng(7)
+    o, w = _oracle_path(9)
+    hit, cs, _ = _random_case(rng, o)
+    bh = np.arange(1, int(o.blk_off[-1]) + 1, dtype=np.uint64) * np.uint64(0x2545F4914F6CDD1D)
+    free = np.arange(w.num_slots, dtype=np.int32)[::-1].copy()
+    R = w.num_reqs
+    a = kv.kv_build_jobs(hit, cs, bh, o.blk_off, o.chunk_off, o.bpc, free)
+    b = kv.kv_build_jobs_routed(hit, cs, bh, o.blk_off, o.chunk_off, o.bpc, free, np.ones(R, bool),
+                                np.full(R, kv.KV_COMMIT, np.int32))
+    assert np.array_equal(a[0], b[0]) and b[1].size == 0
+    assert np.array_equal(a[1], b[2]) and np.array_equal(a[2], b[3]) and a[3] == b[4]
+
+
+def test_routed_rejects_undecided_running_request():
+    o, w = _oracle_path(3)
+    R = w.num_reqs
+    hit = np.zeros(R, np.int32)
+    cs = np.full(int(o.chunk_off[-1]), -1, np.int32)
+    bh = np.zeros(int(o.blk_off[-1]), np.uint64)
+    with pytest.raises(kv.KvError):
+        kv.kv_build_jobs_routed(hit, cs, bh, o.blk_off, o.chunk_off, o.bpc, np.zeros(0, np.int32),
+                                np.ones(R, bool), np.full(R, kv.KV_BLOCKED, np.int32))
+
+
+def test_decide_claims_argument_errors():
+    hit = np.array([1], np.int32)
+    co = np.array([0, 2], np.int64)
+    with pytest.raises(kv.KvError):   # matched slot outside the staging buffer
+        kv.kv_decide_claims(hit, np.array([5, -1], np.int32), co, 0, 0, True, SB, SB, 4)
+    with pytest.raises(kv.KvError):   # hit count beyond the request's chunks
+        kv.kv_decide_claims(np.array([3], np.int32), np.array([0, 1], np.int32), co, 0, 0, True, SB, SB, 4)
+    d, _, _ = kv.kv_decide_claims(hit, np.array([0, -1], np.int32), co, math.nan, 0, True, SB, SB, 4)
+    assert d.tolist() == [kv.KV_EINVAL]
+
+
+# ---------------------------------------------------------------------------
+# TTR estimators
+# ---------------------------------------------------------------------------
+
+def test_oracle_ttr_static_closed_form():
+    b = [3e9, 5e9, 7e9]
+    assert ctl.ttr_static_of([0, 1, 2], b, [False, True, False], 2e9) == (3e9 + 7e9) / 2e9
+    assert ctl.ttr_static_of([1], b, [False, True, False], 2e9) == 0.0
+
+
+def test_oracle_ttr_state_aware_closed_forms():
+    b = [4e9, 2e9, 6e9]
+    res, q, ready = [False] * 3, [False] * 3, [0.0] * 3
+    # idle device: objects back to back from now; equals the static estimate at the same rate
+    assert ctl.ttr_state_aware_of([0, 1, 2], b, res, q, ready, 10.0, 3.0, 2e9) == (4e9 + 2e9 + 6e9) / 2e9
+    # busy until 12 s: everything starts then
+    assert ctl.ttr_state_aware_of([0, 1], b, res, q, ready, 10.0, 12.0, 2e9) == 2.0 + 3.0
+    # object 2 already queued and ready at 30 s decides over the appended ones
+    assert ctl.ttr_state_aware_of([0, 2], b, res, [False, False, True], [0, 0, 30.0], 10.0, 12.0, 2e9) == 20.0
+    # a queued object that finishes before the appended ones does not
+    assert ctl.ttr_state_aware_of([0, 2], b, res, [False, False, True], [0, 0, 11.0], 10.0, 10.0, 2e9) == 2.0
+    # all resident: ready now
+    assert ctl.ttr_state_aware_of([0, 1], b, [True, True, True], q, ready, 10.0, 50.0, 2e9) == 0.0
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_ttr_estimators_match_oracle(seed):
+    rng = np.random.default_rng(seed)
+    O = int(rng.integers(1, 40))
+    b = (rng.integers(0, 64, O) * 2**26).astype(np.float64)
+    res = rng.random(O) < 0.3
+    q = rng.random(O) < 0.3
+    ready = rng.uniform(0, 20, O)
+    objs = rng.permutation(O)[:int(rng.integers(0, O + 1))].tolist()
+    now, busy = float(rng.uniform(0, 10)), float(rng.uniform(0, 15))
+    rate = float(rng.choice([11 * 2**30, 1e9, 3.5e9]))
+    assert kv.kv_ttr_static(objs, b, res, rate) == ctl.ttr_static_of(objs, b, res, rate)
+    assert kv.kv_ttr_state_aware(objs, b, res, q, ready, now, busy, rate) == \
+        ctl.ttr_state_aware_of(objs, b, res, q, ready, now, busy, rate)
+
+
+def test_ttr_argument_errors():
+    with pytest.raises(kv.KvError):
+        kv.kv_ttr_static([3], [1.0, 2.0], [0, 0], 1.0)          # object id out of range
+    with pytest.raises(kv.KvError):
+        kv.kv_ttr_static([0], [1.0], [0], 0.0)                  # rate <= 0
+    with pytest.raises(kv.KvError):
+        kv.kv_ttr_state_aware([0], [1.0], [0], [0], [0.0], math.nan, 0.0, 1.0)

@@ -1,7 +1,15 @@
 """GPU parity at the full workload sizes, in the launch configuration the
 benchmark times.
 
-Buffers of 20-170 GiB cannot be held twice on the host, so:
+Complete comparison, one layer at a time (the 32- and 80-layer batches): for
+every layer the oracle's one-layer walks rebuild the expected paged tensor and
+the expected staging contents from the input formula and the job lists, and
+every byte of the GPU's layer (written blocks, untouched blocks) and of every
+staging slot's part for that layer (stored, read and untouched slots) is
+compared.  Only one layer's buffers per worker are held on the host.
+
+Sampled comparison for every configuration: buffers of 20-170 GiB cannot be
+held twice on the host, so:
   * hash, lookup and the job lists are compared in full with the oracle;
   * copies are checked on sampled segments: for a sampled paged block the
     oracle says (one by one) which staged segment, if any, lands there, and
@@ -9,6 +17,10 @@ Buffers of 20-170 GiB cannot be held twice on the host, so:
     same for sampled staging segments written by the store gather.  Samples
     cover every layer, both planes, the first and last jobs, and blocks that
     no job touches (which must keep their original bytes)."""
+import concurrent.futures as cf
+import os
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -140,3 +152,88 @@ def test_full_size_sampled_pipelined_from_host(name):
 def test_full_size_sampled_quad_retrieve(name):
     # the four-job-window retrieve, which tune_retrieve may choose for a pool
     check_full_size(name, force_kind=kv.KV_RETRIEVE_QUAD)
+
+
+# ---------------------------------------------------------------------------
+# complete comparison, streamed one layer at a time
+# ---------------------------------------------------------------------------
+
+def _layer_check(w, g, o, retr, store, l, bufs):
+    """Compare layer l of the pool and of every staging slot with the oracle's
+    one-layer walks over the formula's bytes.  Returns the bytes compared."""
+    L, S = w.shape.num_layers, w.num_slots
+    part = oracle.layer_part_bytes(o.layout)
+    exp_pool, exp_stg, got_pool, got_stg = bufs
+    # expected: the pool formula with the retrieve's bytes scattered in, then the store's bytes gathered out
+    W.kv_words_np(POOL_TAG + l, w.seed, 0, exp_pool.size // 4, out=exp_pool.view(np.uint32))
+    for s in range(S):
+        W.kv_words_np(STG_TAG, w.seed, (s * w.shape.slot_bytes + l * part) // 4, part // 4,
+                      out=exp_stg[s * part:(s + 1) * part].view(np.uint32))
+    oracle.retrieve_scatter_layer(o.layout, exp_stg, exp_pool, w.block_tables, retr)
+    oracle.store_gather_layer(o.layout, exp_stg, exp_pool, w.block_tables, store)
+    got_pool.copy_(g.layers[l])
+    got_stg.copy_(g.staging.view(S, L, part)[:, l, :].reshape(-1))
+    ok_pool = np.array_equal(got_pool.numpy(), exp_pool)
+    ok_stg = np.array_equal(got_stg.numpy(), exp_stg)
+    assert ok_pool, f"layer {l}: paged tensor differs"
+    assert ok_stg, f"layer {l}: staging differs"
+    return exp_pool.size + exp_stg.size
+
+
+def check_full_size_complete(name, workers=8):
+    w = W.make(name)
+    t0 = time.perf_counter()
+    print(f"[complete] {name}: {w.num_reqs} reqs, pool {w.pool_bytes() / 2**30:.1f} GiB, "
+          f"staging {w.staged_bytes() / 2**30:.1f} GiB", flush=True)
+    g = StagingPath(w)
+    g.fill(STG_TAG, POOL_TAG, w.seed)
+    g.prestage()
+    o = OraclePath(w, with_kv=False)
+    o.prestage()
+    sg, so = g.run_pass(validate=True), o.run_pass()
+    torch.cuda.synchronize()
+    assert np.array_equal(g.last_retrieve, so["retrieve"]) and np.array_equal(g.last_store, so["store"])
+    assert sg.num_retrieve > 0 and sg.num_store > 0
+    retr, store = so["retrieve"], so["store"]
+    L, S = w.shape.num_layers, w.num_slots
+    part = oracle.layer_part_bytes(o.layout)
+    nw = max(1, min(workers, (os.cpu_count() or 4), L))
+    pools = [(np.empty(w.layer_bytes(), np.uint8), np.empty(S * part, np.uint8),
+              torch.from_numpy(np.empty(w.layer_bytes(), np.uint8)),
+              torch.from_numpy(np.empty(S * part, np.uint8))) for _ in range(nw)]
+    free = list(range(nw))
+    total = 0
+
+    def one(l, k):
+        with torch.cuda.stream(torch.cuda.Stream()):
+            n = _layer_check(w, g, o, retr, store, l, pools[k])
+            torch.cuda.current_stream().synchronize()
+        return n
+
+    with cf.ThreadPoolExecutor(nw) as ex:
+        pending = {}
+        for l in range(L):
+            if not free:
+                done, _ = cf.wait(pending, return_when=cf.FIRST_COMPLETED)
+                for f in done:
+                    total += f.result()
+                    free.append(pending.pop(f))
+            k = free.pop()
+            pending[ex.submit(one, l, k)] = k
+        for f in cf.as_completed(pending):
+            total += f.result()
+    print(f"[complete] {name}: {total / 2**30:.1f} GiB compared in {time.perf_counter() - t0:.0f} s", flush=True)
+    del g, pools
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["l32-64x4096", "l80-32x8192"])
+def test_full_size_every_byte(name):
+    check_full_size_complete(name)
+
+
+@pytest.mark.parametrize("name", ["l32-1024x1024-cap50-host", "l32-1024x1024-cap100-host"])
+def test_full_size_sampled_zero_copy_from_host(name):
+    # the capacity sweep's host-staged points in the bench's default zero-copy mode
+    check_full_size(name, lower_tier="zero-copy")

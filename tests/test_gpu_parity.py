@@ -42,6 +42,8 @@ def _compare_pass(g, o, sg, so, check_kv=True):
     assert np.array_equal(g.h_chunk_slot.numpy()[:nch], so["chunk_slot"])
     assert np.array_equal(g.h_hit.numpy()[:R], so["hit"])
     assert np.array_equal(g.last_retrieve, so["retrieve"])
+    assert np.array_equal(g.last_ordinary, so["ordinary"])
+    assert np.array_equal(g.last_decisions, so["decisions"])
     assert np.array_equal(g.last_store, so["store"])
     assert sg.dropped == so["dropped"]
     if check_kv:

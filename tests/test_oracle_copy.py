@@ -236,3 +236,31 @@ def test_bit_patterns_are_opaque():
     back = np.zeros_like(staging)
     oracle.store_gather(lo, back, [layer], bt, jobs)
     assert np.array_equal(back, staging)
+
+
+@pytest.mark.parametrize("shape_args,layout", list(itertools.product(SHAPES, LAYOUTS)))
+def test_one_layer_walks_agree_with_full_walks(shape_args, layout):
+    # the one-layer forms (used for complete checks at full size, one layer at a time) give, layer by layer,
+    # what the full walks give, including skipped jobs and blocks and a slot read by several jobs
+    shape, lo, bt, staging, layers, nb = _setup(61, *shape_args, layout)
+    bt = bt.copy()
+    bt[1, 0] = -1
+    bt[2, 1] = nb
+    L, S = shape.num_layers, lo.num_slots
+    part = oracle.layer_part_bytes(lo)
+    assert part * L == shape.slot_bytes
+    retr = np.array([[4, 0, 0, 0], [1, 2, 1, 0], [4, 1, 2, 0], [0, 1, 0, 0], [9, 0, 1, 0], [2, 0, 7, 0]], np.int32)
+    store = np.array([[5, 2, 2, 0], [3, 1, 1, 0], [0, 0, 2, 0], [1, 5, 0, 0]], np.int32)
+    full = [a.copy() for a in layers]
+    oracle.retrieve_scatter(lo, staging, full, bt, retr)
+    st_full = staging.copy()
+    oracle.store_gather(lo, st_full, full, bt, store)
+    by_layer = staging.reshape(S, L, part)
+    out_by_layer = st_full.reshape(S, L, part)
+    for l in range(L):
+        stg_l = np.ascontiguousarray(by_layer[:, l, :])
+        paged = layers[l].copy()
+        oracle.retrieve_scatter_layer(lo, stg_l, paged, bt, retr)
+        assert np.array_equal(paged, full[l]), l
+        oracle.store_gather_layer(lo, stg_l, paged, bt, store)
+        assert np.array_equal(stg_l, out_by_layer[:, l, :]), l

@@ -62,7 +62,13 @@ MUTANTS = [
      "                        for (int64_t x = 0; x < HD; x++)\n                            for (int32_t c = 0; c < lo->e; c++) {\n"
      "                                int64_t src = jb->slot"),
     ("job_chunk_bound", COPY, "((int64_t)jb->chunk + 1) * nseg > bt_stride", "(int64_t)jb->chunk * nseg > bt_stride"),
-    ("gather_kv_stride_dropped", COPY, "int64_t src = kv * lo->kv_stride + blk * lo->block_stride", "int64_t src = blk * lo->block_stride"),
+    ("gather_kv_stride_dropped", COPY, "\n                                int64_t src = kv * lo->kv_stride + blk * lo->block_stride",
+     "\n                                int64_t src = blk * lo->block_stride"),
+    ("layer_scatter_plane_dropped", COPY, "int64_t src = jb->slot * part_bytes\n                                + (((int64_t)kv * lo->C",
+     "int64_t src = jb->slot * part_bytes\n                                + (((int64_t)0 * lo->C"),
+    ("layer_gather_block_stride_dropped", COPY, "\n                            int64_t src = kv * lo->kv_stride + blk * lo->block_stride",
+     "\n                            int64_t src = kv * lo->kv_stride + (blk / 2) * lo->block_stride"),
+
     ("gather_segment_off_by_one", COPY, "+ ((((int64_t)l * 2 + kv) * lo->C + (int64_t)i * lo->B + t) * HD + x) * lo->e + c;\n"
      "                                int64_t src", "+ ((((int64_t)l * 2 + kv) * lo->C + (int64_t)(i + 1) % nseg * lo->B + t) * HD + x) * lo->e + c;\n"
      "                                int64_t src"),
@@ -135,9 +141,9 @@ CTRL_MUTANTS = [
     ("release_keeps_reservation", "                    if prot[o] == 0:\n                        P -= obj_bytes[o]",
      "                    if prot[o] == 0 and False:\n                        P -= obj_bytes[o]"),
     ("stage_reads_not_coalesced", "if not resident[o] and not queued[o]:\n                start", "if not resident[o]:\n                start"),
-    ("state_ttr_ignores_queue", "        tail = max(busy_until, now)", "        tail = now"),
-    ("state_ttr_first_object_decides", "                tail = tail + obj_bytes[o] / cfg.stage_rate\n                t_end = max(t_end, tail)",
-     "                tail = tail + obj_bytes[o] / cfg.stage_rate\n                t_end = tail if t_end == now else t_end"),
+    ("state_ttr_ignores_queue", "    tail = max(busy_until, now)", "    tail = now"),
+    ("state_ttr_first_object_decides", "            tail = tail + obj_bytes[o] / stage_rate\n            t_end = max(t_end, tail)",
+     "            tail = tail + obj_bytes[o] / stage_rate\n            t_end = tail if t_end == now else t_end"),
     ("tempo_uses_static_ttr", "            ttu, ttr = (ttu_map[i] if i in ttu_map else math.inf), ttr_state(i)",
      "            ttu, ttr = (ttu_map[i] if i in ttu_map else math.inf), ttr_static(i)"),
     ("ttu_ignores_busy_slots", "        slots = [projected_end(a) for a in active] + [now] * (cfg.max_active - len(active))",
@@ -178,4 +184,44 @@ def test_controller_unplanted_copy_passes_the_pins(tmp_path):
     path.write_text(open(CTRL_SRC).read())
     r = subprocess.run([sys.executable, "-c", _RUNNER, str(path), *CTRL_PINS], cwd=ROOT, capture_output=True,
                        text=True, timeout=600)
+    assert r.returncode == 0, r.stdout[-3000:]
+
+
+# ---------------------------------------------------------------------------
+# The oracle's commitment decisions over a batch of claims (oracle/pipeline.py):
+# planted copies loaded in place of oracle.pipeline, against the closed-form
+# pins of tests/test_claims.py (the "oracle_" tests).
+# ---------------------------------------------------------------------------
+PIPE_SRC = os.path.join(ROOT, "oracle", "pipeline.py")
+_PIPE_RUNNER = _RUNNER.replace("oracle.controller", "oracle.pipeline").replace(
+    "'-p', 'no:cacheprovider',", "'-p', 'no:cacheprovider', '-k', 'oracle_',")
+
+PIPE_MUTANTS = [
+    ("claims_in_request_order", "        order = [r for r in range(R) if requested[r]] + [r for r in range(R) if not requested[r]]",
+     "        order = list(range(R))"),
+    ("claims_shared_counted_twice", "            new = sum(slot_bytes for s in objs if s not in protected)",
+     "            new = total"),
+    ("claims_reservations_not_kept", "                reserved += new", "                reserved += 0"),
+    ("claims_free_ignores_reservations", "            free = max(claims.budget_bytes - reserved, 0)",
+     "            free = claims.budget_bytes"),
+    ("claims_blocked_stops_walk", "            decision[r] = d\n", "            decision[r] = d\n            if d != oracle.COMMIT:\n                break\n"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", PIPE_MUTANTS, ids=[m[0] for m in PIPE_MUTANTS])
+def test_claim_pins_catch_planted_mistake(tmp_path, name, old, new):
+    src = open(PIPE_SRC).read()
+    assert src.count(old) == 1, f"{name}: the text to change must occur exactly once"
+    path = tmp_path / "pipeline.py"
+    path.write_text(src.replace(old, new))
+    r = subprocess.run([sys.executable, "-c", _PIPE_RUNNER, str(path), "tests/test_claims.py"], cwd=ROOT,
+                       capture_output=True, text=True, timeout=600)
+    assert r.returncode == 1 or r.returncode < 0, f"{name} survived the pins:\n{r.stdout[-2000:]}"
+
+
+def test_claim_pins_pass_on_unplanted_copy(tmp_path):
+    path = tmp_path / "pipeline.py"
+    path.write_text(open(PIPE_SRC).read())
+    r = subprocess.run([sys.executable, "-c", _PIPE_RUNNER, str(path), "tests/test_claims.py"], cwd=ROOT,
+                       capture_output=True, text=True, timeout=600)
     assert r.returncode == 0, r.stdout[-3000:]
