@@ -14,13 +14,17 @@ steps, and outside the timed region, the retrieve variant for this pool is
 chosen by timing the planned one against the four-job-window one (--no-tune
 keeps the plan).
 
-Prints one JSON line: the whole-step payload rate in GB/s (bytes read plus
-bytes written by the scatter and the gather, divided by wall time per step),
-per-kernel rates measured with HIP events on the launch stream, the roofline
-of the dominant copy kernel against MI355X's 8 TB/s HBM peak, and the CPU
-oracle timed on a bounded sample of the same workload shape.
+Prints one JSON line: the whole step's HBM bytes per second (the
+retrieve's unique staged reads and its writes plus the store's reads and
+writes, divided by wall time per step; the payload rate, which counts every
+job's read, is reported beside it), per-kernel rates measured with HIP events
+on the launch stream, the roofline of the dominant copy kernel against
+MI355X's 8 TB/s HBM peak (both copy kernels are listed), same-pool ceilings,
+and the CPU oracle timed on a bounded sample of the same workload shape.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME]
+    python bench.py --summarize-trace DIR --workload NAME --command CMD   (rocprofv3 output -> profiles/)
+    python bench.py --summarize-traffic DIR --workload NAME               (FETCH_SIZE / WRITE_SIZE -> profiles/)
 """
 from __future__ import annotations
 
@@ -48,10 +52,14 @@ def _src_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def _load_traffic(kernel: str, workload: str):
+def _load_traffic(kernel: str, workload: str, variant: str = None):
     """HBM bytes per launch measured by rocprofv3 counters, if a summary for
-    this kernel and workload exists and was taken from the current source."""
-    path = os.path.join(PROFILES, f"traffic_{kernel}_{workload}.txt")
+    this kernel (retrieve: and variant) and workload exists and was taken from
+    the current source."""
+    if kernel == "kv_copy_retrieve" and variant is None:
+        return None
+    tag = f"{kernel}_{variant}" if kernel == "kv_copy_retrieve" else kernel
+    path = os.path.join(PROFILES, f"traffic_{tag}_{workload}.txt")
     if not os.path.exists(path):
         return None
     kvs = {}
@@ -65,6 +73,238 @@ def _load_traffic(kernel: str, workload: str):
         return float(kvs["traffic_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+# ---------------------------------------------------------------------------
+# Kernel symbols, and the summaries of rocprofv3 output committed under profiles/
+# ---------------------------------------------------------------------------
+
+def _rows_of(seg_bytes: int, row_bytes: int) -> int:
+    """Rows of `row_bytes` per segment when that is 1, 2, 4, 8 or 16 (the copy kernels' fast paths)."""
+    if seg_bytes % row_bytes:
+        return 0
+    r = seg_bytes // row_bytes
+    return r if r in (1, 2, 4, 8, 16) else 0
+
+
+def _symbol(kind: str, w) -> str:
+    """The __global__ function (copy.hip) a copy launch of this kind runs for the workload's segment size."""
+    seg = w.shape.seg_bytes
+    if kind in ("unit", "pair", "quad"):
+        r = _rows_of(seg, 256 * 16)
+        if kind == "pair" and r != 8:
+            kind = "unit"
+        if r:
+            return {"unit": "retrieve_unit_kernel", "pair": "retrieve_pair_kernel",
+                    "quad": "retrieve_quad_kernel"}[kind] + f"<{r}>"
+        return "copy_generic_kernel<true>"
+    retrieve = kind == "stream"
+    for t in (1024, 512, 256):
+        r = _rows_of(seg, t * 16)
+        if r:
+            return f"group_copy_kernel<{t}, {r}, {'true' if retrieve else 'false'}>"
+    return f"copy_generic_kernel<{'true' if retrieve else 'false'}>"
+
+
+def _label(symbol: str) -> str:
+    """What a library kernel does, from its symbol."""
+    for key, text in (("retrieve_unit_kernel", "retrieve scatter, unit walk (KV_RETRIEVE_UNIT)"),
+                      ("retrieve_pair_kernel", "retrieve scatter, pair walk (KV_RETRIEVE_PAIR)"),
+                      ("retrieve_quad_kernel", "retrieve scatter, four-job window (KV_RETRIEVE_QUAD)"),
+                      ("copy_generic_kernel<true>", "retrieve scatter, generic path"),
+                      ("copy_generic_kernel<false>", "store gather, generic path"),
+                      ("hash_kernel", "prefix hash (kv_hash_prefix)"),
+                      ("lookup_kernel", "lookup (kv_lookup)"),
+                      ("index_apply_kernel", "index update (kv_index_insert / erase)")):
+        if key in symbol:
+            return text
+    if "group_copy_kernel" in symbol:
+        return ("retrieve scatter, streaming (KV_RETRIEVE_STREAM)" if "true>" in symbol
+                else "store gather (kv_store_gather)")
+    return "other"
+
+
+def _short_symbol(name: str) -> str:
+    """rocprofv3's demangled kernel name without namespaces and argument list."""
+    base = name.split("(tkv::")[0].split("(long")[0].split("(const")[0]
+    if base.endswith(")") and "(" in base and "<" not in base.split("(")[-1]:
+        base = base[:base.rfind("(")]
+    base = base.replace("tkv::(anonymous namespace)::", "").replace("(anonymous namespace)::", "").strip()
+    return base[5:] if base.startswith("void ") else base
+
+
+def _csv_rows(directory: str, suffix: str):
+    import csv
+    import glob
+    files = sorted(glob.glob(os.path.join(directory, "**", f"*{suffix}"), recursive=True))
+    if not files:
+        raise FileNotFoundError(f"no *{suffix} under {directory}")
+    rows = []
+    for f in files:
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def _bench_json(log: str):
+    if not os.path.exists(log):
+        return None
+    js = [l for l in open(log) if l.startswith("{")]
+    return json.loads(js[-1]) if js else None
+
+
+def profile_commands(workload: str, out: str) -> list:
+    """The rocprofv3 runs behind profiles/*_{workload}.*: (name, command) pairs,
+    each writing under `out`/name (every counter pass is a run of its own)."""
+    b3 = f"python3 bench.py --steps 3 --warmup 1 --no-fill --workload {workload}"
+    pmc = {"sq": "SQ_INSTS_VMEM_RD SQ_INSTS_VMEM_WR SQ_INSTS_SMEM SQ_WAVES SQ_INSTS_VALU SQ_INSTS_SALU "
+                 "SQ_BUSY_CYCLES SQ_WAVE_CYCLES",
+           "tcc": "TCC_HIT_sum TCC_MISS_sum TCC_EA0_WRREQ_sum TCC_EA0_RDREQ_sum",
+           "tlb": "TCP_UTCL1_TRANSLATION_MISS_sum TCP_UTCL1_TRANSLATION_HIT_sum GRBM_GUI_ACTIVE GRBM_COUNT",
+           "occ": "OccupancyPercent",
+           "pmc_fetch": "FETCH_SIZE", "pmc_write": "WRITE_SIZE"}
+    cmds = [("ktrace", f"rocprofv3 --kernel-trace --stats -f csv -d {out}/ktrace -o c -- python3 bench.py "
+                       f"--no-cpu-baseline --no-extras --workload {workload}")]
+    for name, ctrs in pmc.items():
+        cmds.append((name, f"rocprofv3 --pmc {ctrs} --kernel-include-regex tkv -f csv -d {out}/{name} -o c -- {b3}"))
+    for name, ctr in (("cal_fetch", "FETCH_SIZE"), ("cal_write", "WRITE_SIZE")):
+        cmds.append((name, f"rocprofv3 --pmc {ctr} -f csv -d {out}/{name} -o c -- python3 bench.py --calib-copy"))
+    return cmds
+
+
+def summarize_trace(directory: str, workload: str, command: str) -> str:
+    """profiles/kernel_trace_{workload}.md from a rocprofv3 --kernel-trace --stats run."""
+    rows = _csv_rows(directory, "_kernel_stats.csv")
+    lines = [f"# Kernel trace summary: {workload}", "", "Command (repository root, one MI355X):", "", "```", command,
+             "```", "", "Made by `python bench.py --summarize-trace`: the rows of rocprofv3's kernel statistics whose "
+             "kernel is one of the library's, with the kernel's symbol as rocprofv3 printed it "
+             "(namespaces and argument list dropped); all other rows are the input generator and runtime copies.",
+             "", "| kernel | symbol (copy.hip, hash.hip, index.hip) | calls | avg us | min us | max us | total ms |",
+             "|---|---|---:|---:|---:|---:|---:|"]
+    ours = [r for r in rows if _label(_short_symbol(r["Name"])) != "other"]
+    for r in sorted(ours, key=lambda r: -float(r["TotalDurationNs"])):
+        sym = _short_symbol(r["Name"])
+        lines.append(f"| {_label(sym)} | `{sym}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
+                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.2f} |")
+    other = [r for r in rows if _label(_short_symbol(r["Name"])) == "other"]
+    lines += ["", f"Other kernels: {len(other)} names, "
+                  f"{sum(float(r['TotalDurationNs']) for r in other) / 1e6:.1f} ms in total."]
+    d = _bench_json(os.path.join(directory, "bench.log"))
+    if d:
+        k = d["kernels"]
+        tun = d["config"].get("retrieve_tuning_ms") or {}
+        lines += ["", f"The timed steps ran the `{d['config'].get('retrieve_variant')}` retrieve "
+                      f"(`{d['roofline']['per_kernel']['retrieve_scatter']['symbol']}`)."]
+        if tun:
+            lines[-1] += (" Before them the bench timed the candidates on this pool (medians: "
+                          + ", ".join(f"{n} {v:.3f} ms" for n, v in tun.items()) + "), so both appear above.")
+        lines += ["", "HIP-event timings the same run printed (mean over its timed steps): "
+                      f"retrieve {k['retrieve_scatter']['ms']:.3f} ms, store {k['store_gather']['ms']:.3f} ms; "
+                      f"hash {k['hash_prefix'].get('isolated_ms', 0) * 1e3:.1f} us and lookup "
+                      f"{k['lookup'].get('isolated_ms', 0) * 1e3:.1f} us on an idle GPU."]
+    path = os.path.join(PROFILES, f"kernel_trace_{workload}.md")
+    open(path, "w").write("\n".join(lines) + "\n")
+    return path
+
+
+def _counter_medians(directory: str):
+    import statistics
+    from collections import defaultdict
+    agg = defaultdict(list)
+    for r in _csv_rows(directory, "_counter_collection.csv"):
+        agg[(_short_symbol(r["Kernel_Name"]), r["Counter_Name"])].append(float(r["Counter_Value"]))
+    return {k: statistics.median(v) for k, v in agg.items()}
+
+
+def summarize_traffic(directory: str, workload: str, calibration: str = None) -> list:
+    """profiles/traffic_*_{workload}.txt: FETCH_SIZE and WRITE_SIZE per launch
+    of the store and of the retrieve variant the timed steps ran, scaled by
+    what the same counters read for the calibration copy of known size."""
+    w_cal = 4 << 30
+    cal_dir = calibration or directory
+    cmds = dict(profile_commands(workload, "gpurun_out/prof_" + workload))
+    cal_wl = os.path.basename(os.path.normpath(cal_dir))[len("prof_"):] or workload
+    cmds.update({k: v for k, v in profile_commands(cal_wl, "gpurun_out/prof_" + cal_wl) if k.startswith("cal_")})
+    fe, wr = _counter_medians(os.path.join(directory, "pmc_fetch")), _counter_medians(os.path.join(directory, "pmc_write"))
+    cf = [v for (k, c), v in _counter_medians(os.path.join(cal_dir, "cal_fetch")).items() if "copy_generic" in k]
+    cw = [v for (k, c), v in _counter_medians(os.path.join(cal_dir, "cal_write")).items() if "copy_generic" in k]
+    f_fetch, f_write = w_cal / 1024 / cf[0], w_cal / 1024 / cw[0]
+    d = _bench_json(os.path.join(directory, "pmc_fetch.log"))
+    variant = d["config"]["retrieve_variant"]
+    import workloads as W
+    w = W.make(workload)
+    out = []
+    kinds = [("kv_copy_store", _symbol("store", w))]
+    for v in ("unit", "pair", "quad", "stream"):
+        # the timed variant, and the candidate the retrieve tuning also launched in the same run
+        if _symbol(v, w) not in [k for k, _ in kinds]:
+            kinds.append((f"kv_copy_retrieve_{v}", _symbol(v, w)))
+    for kern, sym in kinds:
+        fk = [v for (k, c), v in fe.items() if k == sym and c == "FETCH_SIZE"]
+        wk = [v for (k, c), v in wr.items() if k == sym and c == "WRITE_SIZE"]
+        if not fk or not wk:
+            continue
+        fk, wk = fk[0], wk[0]
+        txt = [f"# HBM traffic per launch of {_label(sym)}, workload {workload}",
+               "# Made by `python bench.py --summarize-traffic` from these runs (repository root, one MI355X):",
+               *[f"#   {cmds[n]}" for n in ("pmc_fetch", "pmc_write", "cal_fetch", "cal_write")],
+               "# Each counter is the median over the kernel's launches, in KiB per dispatch, scaled by the same",
+               "# counter's reading for the calibration: a 4 GiB contiguous copy (4 GiB read, 4 GiB written) by",
+               "# copy_generic_kernel<true>.  --no-fill: the KV buffers are not initialised (the copies move the",
+               "# same bytes); the input fill is never run under --pmc.",
+               f"kernel={kern}", f"symbol={sym}", f"workload={workload}", f"source_digest={_src_digest()}",
+               f"timed_variant={variant}" + ("" if kern == "kv_copy_store" or kern.endswith(variant) else
+                                              " (this variant ran in the retrieve tuning before the timed steps)"),
+               f"fetch_kib_per_dispatch={fk:.1f}", f"write_kib_per_dispatch={wk:.1f}",
+               f"calibration_fetch_kib={cf[0]:.1f}", f"calibration_write_kib={cw[0]:.1f}",
+               f"fetch_scale={f_fetch:.4f}", f"write_scale={f_write:.4f}",
+               f"hbm_read_bytes_per_launch={fk * f_fetch * 1024:.0f}",
+               f"hbm_write_bytes_per_launch={wk * f_write * 1024:.0f}",
+               f"traffic_bytes_per_launch={(fk * f_fetch + wk * f_write) * 1024:.0f}"]
+        path = os.path.join(PROFILES, f"traffic_{kern}_{workload}.txt")
+        open(path, "w").write("\n".join(txt) + "\n")
+        out.append(path)
+    return out
+
+
+def summarize_counters(directory: str, workload: str) -> str:
+    """profiles/counters_{workload}.md: memory instructions, L2 traffic and hit
+    rate, address translation and occupancy per launch of each copy kernel."""
+    cmds = dict(profile_commands(workload, "gpurun_out/prof_" + workload))
+    c = {}
+    for kind in ("sq", "tcc", "tlb", "occ"):
+        c.update(_counter_medians(os.path.join(directory, kind)))
+    d = _bench_json(os.path.join(directory, "sq.log"))
+    lines = [f"# Hardware counters per launch: workload {workload}", "",
+             "Commands (repository root, one MI355X; one counter group per run):", "", "```",
+             *[cmds[k] for k in ("sq", "tcc", "tlb", "occ")], "```", "",
+             "Made by `python bench.py --summarize-counters`: medians over each kernel's launches.  "
+             "TCC_EA0_RDREQ counts 128-byte and TCC_EA0_WRREQ 64-byte requests leaving the L2 (hits in the memory-side "
+             "cache included).  --no-fill: KV buffers uninitialised, same bytes moved."]
+    if d:
+        lines[-1] += (f"  The timed steps ran the `{d['config'].get('retrieve_variant')}` retrieve; the tuning before "
+                      "them launches both candidates, so both appear.")
+    syms = sorted({k for (k, cn) in c if cn == "SQ_WAVES" and _label(k) != "other"})
+    for sym in syms:
+        g = lambda n, sym=sym: c.get((sym, n), float("nan"))
+        waves = g("SQ_WAVES")
+        hit, miss = g("TCC_HIT_sum"), g("TCC_MISS_sum")
+        th, tm = g("TCP_UTCL1_TRANSLATION_HIT_sum"), g("TCP_UTCL1_TRANSLATION_MISS_sum")
+        lines += ["", f"## {_label(sym)}: `{sym}`", "", "| quantity | value | per wave or bytes |", "|---|---:|---|",
+                  f"| SQ_WAVES | {waves:.0f} | |",
+                  f"| SQ_INSTS_VMEM_RD | {g('SQ_INSTS_VMEM_RD'):.0f} | x 1 KiB = {g('SQ_INSTS_VMEM_RD') * 1024 / 1e9:.3f} GB |",
+                  f"| SQ_INSTS_VMEM_WR | {g('SQ_INSTS_VMEM_WR'):.0f} | x 1 KiB = {g('SQ_INSTS_VMEM_WR') * 1024 / 1e9:.3f} GB |",
+                  f"| SQ_INSTS_SMEM | {g('SQ_INSTS_SMEM'):.0f} | {g('SQ_INSTS_SMEM') / waves:.1f} per wave |",
+                  f"| SQ_INSTS_VALU / SQ_INSTS_SALU | {g('SQ_INSTS_VALU'):.0f} / {g('SQ_INSTS_SALU'):.0f} | "
+                  f"{g('SQ_INSTS_VALU') / waves:.0f} / {g('SQ_INSTS_SALU') / waves:.0f} per wave |",
+                  f"| TCC_EA0_RDREQ_sum | {g('TCC_EA0_RDREQ_sum'):.0f} | x 128 B = {g('TCC_EA0_RDREQ_sum') * 128 / 1e9:.3f} GB |",
+                  f"| TCC_EA0_WRREQ_sum | {g('TCC_EA0_WRREQ_sum'):.0f} | x 64 B = {g('TCC_EA0_WRREQ_sum') * 64 / 1e9:.3f} GB |",
+                  f"| L2 hit rate | {hit / (hit + miss) * 100:.1f} % | TCC_HIT_sum {hit:.0f}, TCC_MISS_sum {miss:.0f} |",
+                  f"| UTCL1 translation misses | {tm:.0f} | of {th + tm:.0f} ({tm / (th + tm) * 100:.3f} %) |",
+                  f"| OccupancyPercent | {g('OccupancyPercent'):.1f} % | |"]
+    path = os.path.join(PROFILES, f"counters_{workload}.md")
+    open(path, "w").write("\n".join(lines) + "\n")
+    return path
 
 
 def _cpu_baseline(shape):
@@ -148,9 +388,89 @@ def _retrieve_write_bound(path, torch, reps: int = 5):
         ms.append(a.elapsed_time(b))
     t = float(np.median(ms))
     written = n * w.shape.slot_bytes
-    return {"ms": round(t, 4), "GB/s_written": round(written / (t * 1e-3) / 1e9, 1),
-            "what": "the timed retrieve's jobs and variant with every job reading one staged chunk: its "
-                    "scattered writes alone (median of 5)"}
+    out = {"ms": round(t, 4), "GB/s_written": round(written / (t * 1e-3) / 1e9, 1),
+           "what": "the timed retrieve's jobs and variant with every job reading one staged chunk: its "
+                   "scattered writes alone (median of 5)"}
+    # The same writes with the unique staged chunks read from HBM at the same time, on a second stream:
+    # the retrieve's algorithmic bytes (unique reads + writes) with no kernel of ours reading them.  The
+    # reads are torch reductions over the contiguous runs of the chunks' slots.
+    slots = np.unique(path.h_retr.numpy()[:n, 0])
+    runs, start = [], int(slots[0])
+    for prev, cur in zip(slots[:-1], slots[1:]):
+        if cur != prev + 1:
+            runs.append((start, int(prev) + 1))
+            start = int(cur)
+    runs.append((start, int(slots[-1]) + 1))
+    sb = w.shape.slot_bytes
+    views = [path.staging[r0 * sb:r1 * sb].view(torch.int64) for r0, r1 in runs]
+    uniq = int(slots.size) * sb
+    s2 = torch.cuda.Stream()
+    sink = torch.zeros(len(views), dtype=torch.int64, device=path.dev)
+
+    def read_unique(stream):
+        with torch.cuda.stream(stream):
+            for k, v in enumerate(views):
+                torch.sum(v, dim=0, out=sink[k])
+
+    rd, mixed = [], []
+    for _ in range(reps):
+        a.record(s)
+        read_unique(s)
+        b.record(s)
+        b.synchronize()
+        rd.append(a.elapsed_time(b))
+        c = torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        s2.wait_event(a)
+        read_unique(s2)
+        kv.kv_retrieve_scatter_as(path.retrieve_kind, path.layout, path.staging_ptr, path.layers, path.bt,
+                                  w.bt_stride, w.num_reqs, d_jobs, n, s)
+        c.record(s2)
+        s.wait_event(c)
+        b.record(s)
+        b.synchronize()
+        mixed.append(a.elapsed_time(b))
+    t_rd, t_mx = float(np.median(rd)), float(np.median(mixed))
+    out["unique_read"] = {"ms": round(t_rd, 4), "GB/s": round(uniq / (t_rd * 1e-3) / 1e9, 1),
+                          "what": "the retrieve's unique staged chunks read once (torch reductions), idle GPU"}
+    out["writes_with_unique_read"] = {
+        "ms": round(t_mx, 4), "GB/s_alg": round((uniq + written) / (t_mx * 1e-3) / 1e9, 1),
+        "what": "the scattered writes alone and the unique reads, concurrently on two streams (median of 5): "
+                "the retrieve's algorithmic bytes on this pool without the retrieve's own reads"}
+    return out
+
+
+def _store_shape_copy(torch, reps: int = 5) -> dict:
+    """A plain contiguous copy run by the store gather's own kernel shape
+    (1024-lane workgroups, 16 non-temporal 16-byte loads per lane, then the
+    stores): one layer, 8 heads x 128 dims bf16, 16-token blocks, 256-token
+    chunks, the [2][NB][B][H][D] paged layout and an identity block table, so
+    that each staged chunk's K and V halves are 512 KiB contiguous runs of the
+    paged tensor.  4 GiB read and 4 GiB written per launch: the practical
+    ceiling of a dense copy in the shape the store runs."""
+    import numpy as np
+    import paper_2609_35065_amd as kv
+    n, seg = 4096, 16 * 8 * 128 * 2            # 4096 chunks of 1 MiB; 32 KiB segments
+    nb = 16 * n
+    lo = kv.make_layout(1, 8, 128, 2, 16, 256, nb, n, nb * seg, seg)
+    stg = torch.empty(n * 32 * seg, dtype=torch.uint8, device="cuda")
+    pool = torch.empty(2 * nb * seg, dtype=torch.uint8, device="cuda")
+    bt = torch.from_numpy(np.arange(nb, dtype=np.int32).reshape(n, 16)).cuda()
+    jobs = torch.from_numpy(np.stack([np.arange(n), np.arange(n), np.zeros(n), np.zeros(n)], 1)
+                            .astype(np.int32)).cuda()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    kv.kv_store_gather(lo, stg, [pool], bt, 16, n, jobs, n)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        kv.kv_store_gather(lo, stg, [pool], bt, 16, n, jobs, n)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    del stg, pool
+    torch.cuda.empty_cache()
+    return {"ms": round(ms, 4), "GB/s_rw": round(2 * n * 32 * seg / (ms * 1e-3) / 1e9, 1),
+            "what": "4 GiB contiguous copy by the store gather's kernel (1024-lane workgroups, non-temporal)"}
 
 
 def _calibration_copy(torch, reps: int = 5) -> dict:
@@ -177,7 +497,8 @@ def _calibration_copy(torch, reps: int = 5) -> dict:
     e.record()
     torch.cuda.synchronize()
     ms = s.elapsed_time(e) / reps
-    return {"calibration": "contiguous copy by kv_copy_retrieve", "bytes_read_per_dispatch": n * 2 * seg,
+    return {"calibration": "contiguous copy by copy_generic_kernel<true> (the retrieve's generic path, cached "
+                           "loads)", "bytes_read_per_dispatch": n * 2 * seg,
             "bytes_written_per_dispatch": n * 2 * seg, "dispatches": reps + 1, "ms": round(ms, 4),
             "GB/s_rw": round(2 * n * 2 * seg / (ms * 1e-3) / 1e9, 1)}
 
@@ -343,7 +664,38 @@ def main() -> int:
     ap.add_argument("--no-fill", action="store_true",
                     help="leave KV buffers uninitialised (hardware-counter runs: no generator kernels run; the "
                          "copies move the same bytes) and skip the device-copy and CPU-baseline extras")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the same-pool ceilings and practical-peak copies after the timed steps (kernel "
+                         "traces: every launch of a copy kernel is then a step's, a tuning or an idle-GPU pass's)")
+    ap.add_argument("--profile-commands", metavar="OUTDIR",
+                    help="print the rocprofv3 runs behind the profiles of --workload, writing under OUTDIR "
+                         "(name<TAB>command per line), and exit")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="write profiles/kernel_trace_<workload>.md from a rocprofv3 kernel-trace run in DIR "
+                         "(with its bench output in DIR/bench.log) and exit; --command names the run")
+    ap.add_argument("--summarize-traffic", metavar="DIR",
+                    help="write profiles/traffic_*_<workload>.txt from the pmc_fetch, pmc_write, cal_fetch and "
+                         "cal_write runs under DIR and exit")
+    ap.add_argument("--summarize-counters", metavar="DIR",
+                    help="write profiles/counters_<workload>.md from the sq, tcc, tlb and occ runs under DIR and exit")
+    ap.add_argument("--command", default="", help="the command a --summarize-trace run was made with")
+    ap.add_argument("--calibration", default=None,
+                    help="--summarize-traffic: directory holding the cal_fetch / cal_write runs (default: DIR)")
     args = ap.parse_args()
+
+    if args.profile_commands:
+        for name, cmd in profile_commands(args.workload, args.profile_commands):
+            print(f"{name}\t{cmd}")
+        return 0
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace, args.workload, args.command))
+        return 0
+    if args.summarize_traffic:
+        print("\n".join(summarize_traffic(args.summarize_traffic, args.workload, args.calibration)))
+        return 0
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters, args.workload))
+        return 0
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -430,7 +782,7 @@ def main() -> int:
     ms_step = (t1 - t0) * 1e3 / args.steps
     r_bytes = 2 * stats.retrieve_bytes          # read + write per step
     s_bytes = 2 * stats.store_bytes
-    value = (r_bytes + s_bytes) / (ms_step * 1e-3) / 1e9
+    payload_rate = (r_bytes + s_bytes) / (ms_step * 1e-3) / 1e9
     k_ms = {k: avg_ms(k) for k in ("hash", "lookup", "retrieve", "store", "stage")}
     r_gbs = r_bytes / (k_ms["retrieve"] * 1e-3) / 1e9 if k_ms["retrieve"] else 0.0
     s_gbs = s_bytes / (k_ms["store"] * 1e-3) / 1e9 if k_ms["store"] else 0.0
@@ -444,10 +796,22 @@ def main() -> int:
     uniq = len(set(int(q[0]) for q in path.last_retrieve)) * w.shape.slot_bytes
     r_alg = uniq + stats.retrieve_bytes
     r_hbm = r_alg / (k_ms["retrieve"] * 1e-3) / 1e9 if k_ms["retrieve"] else 0.0
+    # the step in HBM bytes: unique staged reads + writes of the retrieve, reads + writes of the store (with
+    # the staging buffer in host memory the retrieve's reads cross the host link instead: payload rate)
+    hbm_rate = (r_alg + s_bytes) / (ms_step * 1e-3) / 1e9
+    value = payload_rate if w.staging_in_host else hbm_rate
     dom = "retrieve" if k_ms["retrieve"] * 1 >= k_ms["store"] else "store"
     dom_kernel = "kv_copy_retrieve" if dom == "retrieve" else "kv_copy_store"
     achieved = r_hbm if dom == "retrieve" else s_gbs
-    traffic = _load_traffic(dom_kernel, args.workload)
+    variant = RETRIEVE_KIND_NAMES.get(path.retrieve_kind)
+    traffic = _load_traffic(dom_kernel, args.workload, variant)
+    per_kernel = {
+        "store_gather": {"symbol": _symbol("store", w), "achieved": round(s_gbs, 1),
+                         "frac": round(s_gbs / HBM_PEAK_GBS, 4), "traffic": _load_traffic("kv_copy_store", args.workload)},
+        "retrieve_scatter": {"symbol": _symbol(variant, w) if variant else None, "achieved": round(r_hbm, 1),
+                             "frac": round(r_hbm / HBM_PEAK_GBS, 4),
+                             "traffic": _load_traffic("kv_copy_retrieve", args.workload, variant)},
+    }
     line = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -467,10 +831,19 @@ def main() -> int:
                    "pool_blocks": w.num_blocks, "staging_slots": w.num_slots,
                    "retrieve_jobs": stats.num_retrieve, "store_jobs": stats.num_store,
                    "steps_overlap": not args.serial,
-                   "retrieve_variant": RETRIEVE_KIND_NAMES.get(path.retrieve_kind),
+                   "retrieve_variant": variant,
                    "retrieve_tuning_ms": tuning},
-        "roofline": {"bound": "hbm", "kernel": dom_kernel, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic},
+        "value_basis": ("payload bytes (staging in host memory) per second of step" if w.staging_in_host else
+                        "HBM bytes per second of step: unique staged reads + writes of the retrieve, reads + "
+                        "writes of the store"),
+        "payload_GB/s": round(payload_rate, 1),
+        "roofline": {"bound": "hbm", "kernel": dom_kernel, "symbol": per_kernel[
+                         "retrieve_scatter" if dom == "retrieve" else "store_gather"]["symbol"],
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "per_kernel": per_kernel,
+                     "min_frac": round(min(v["frac"] for v in per_kernel.values() if v["achieved"]) if any(
+                         v["achieved"] for v in per_kernel.values()) else 0.0, 4)},
         "kernels": {
             "retrieve_scatter": {"ms": round(k_ms["retrieve"], 4), "GB/s": round(r_hbm, 1),
                                  "frac_of_peak": round(r_hbm / HBM_PEAK_GBS, 4), "algorithmic_bytes": r_alg,
@@ -488,8 +861,7 @@ def main() -> int:
         "source_digest": _src_digest(),
     }
     if not w.staging_in_host:
-        # the same step in HBM terms: unique staged reads + writes of the retrieve, reads + writes of the store
-        line["step_hbm_GB/s"] = round((r_alg + s_bytes) / (ms_step * 1e-3) / 1e9, 1)
+        line["step_hbm_GB/s"] = round(hbm_rate, 1)
     for name, key in (("retrieve", "retrieve_scatter"), ("store", "store_gather"), ("hash", "hash_prefix"),
                       ("lookup", "lookup")):
         line["kernels"][key].update(spread(name))
@@ -502,17 +874,23 @@ def main() -> int:
                 lt["stage_ms"] = round(k_ms["stage"], 4)
                 lt["stage_GB/s"] = round(stats.staged_bytes / (k_ms["stage"] * 1e-3) / 1e9, 1)
         line["config"]["lower_tier"] = lt
-    wb = _retrieve_write_bound(path, torch) if not args.no_fill else None
+    extras = not args.no_fill and not args.no_extras
+    wb = _retrieve_write_bound(path, torch) if extras else None
     del path
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
-    if not args.no_fill:
-        line["practical_peak"] = {"torch_device_copy_GB/s": round(_device_copy_gbs(torch), 1),
-                                  "library_contiguous_copy_GB/s": _calibration_copy(torch)["GB/s_rw"]}
+    if extras:
+        sc = _store_shape_copy(torch)
+        line["practical_peak"] = {"store_shape_copy_GB/s": sc["GB/s_rw"],
+                                  "store_frac_of_store_shape_copy": round(s_gbs / sc["GB/s_rw"], 4),
+                                  "torch_device_copy_GB/s": round(_device_copy_gbs(torch), 1),
+                                  "generic_copy_GB/s": _calibration_copy(torch)["GB/s_rw"]}
         if wb:
             # the retrieve's algorithmic bytes moved at the pool's own scattered-write rate
             wb["alg_bytes_at_this_rate_ms"] = round(r_alg / (wb["GB/s_written"] * 1e9) * 1e3, 4)
             wb["retrieve_frac_of_this_rate"] = round(wb["alg_bytes_at_this_rate_ms"] / k_ms["retrieve"], 4)
+            mx = wb["writes_with_unique_read"]
+            mx["retrieve_frac_of_this_ceiling"] = round(mx["ms"] / k_ms["retrieve"], 4)
             line["practical_peak"]["retrieve_writes_only"] = wb
         if w.staging_in_host:
             line["practical_peak"].update(_host_link_gbs(torch))
@@ -521,7 +899,15 @@ def main() -> int:
                        "memory_GiB": round(props.total_memory / 2**30, 1), "clocks": _clocks()}
     if not args.no_cpu_baseline and not args.no_fill:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = _cpu_baseline(w.shape)
+        cb = _cpu_baseline(w.shape)
+        # why a sample: the oracle at this rate would take this long for one whole step of the workload
+        full_s = (r_bytes + s_bytes) / (cb["value"] * 1e9) if cb["value"] else None
+        cb["full_step_estimate_s"] = round(full_s, 1) if full_s else None
+        cb["sample"] += (f"; bounded so that the default run stays within minutes: one whole step of "
+                         f"{w.name} moves {(r_bytes + s_bytes) / 2**30:.0f} GiB, about {full_s:.0f} s of single-core "
+                         f"oracle work per step at this rate, with {w.pool_bytes() / 2**30 + w.staged_bytes() / 2**30:.0f}"
+                         f" GiB of host buffers" if full_s else "")
+        line["cpu_baseline"] = cb
     print(json.dumps(line), flush=True)
     return 0
 
