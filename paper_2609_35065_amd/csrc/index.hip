@@ -1,10 +1,10 @@
 // index.hip -- the staged-chunk index: key -> staging slot.
 //
 // Host policy decides what is staged (job build allocates slots, eviction
-// frees them), so the authoritative table lives on the host; kv_lookup
-// probes a device mirror of it.  Both use the same open-addressing layout
-// (linear probing from a Fibonacci-hashed home position, tombstones for
-// erased keys), so a mutation is mirrored by uploading the table image.
+// frees them), so the authoritative table lives on the host (IndexTable,
+// index_table.cpp); kv_lookup probes a device mirror of it.  Both use the same
+// open-addressing layout, so a mutation is mirrored by uploading the table
+// image.
 //
 // Uploads are stream-ordered, so a lookup enqueued after an insert on the
 // same stream sees the insert.  A mutation that changed few entries uploads
@@ -34,19 +34,11 @@ struct alignas(16) IndexUpdate {
 
 struct kv_index {
     int device = 0;
-    int64_t max_entries = 0;
-    int log2cap = 0;
-    int64_t cap = 0;
-    int64_t live = 0;
-    int64_t tombs = 0;
-    std::vector<tkv::IndexEntry> host;
-    std::vector<tkv::IndexEntry> spare;   // same size as host: a rehash rebuilds into it, then swaps
-    tkv::IndexEntry *dev = nullptr;
+    tkv::IndexTable table;           // the authoritative host table
+    tkv::IndexEntry *dev = nullptr;  // its device mirror
     tkv::IndexEntry *snap[2] = {nullptr, nullptr};
     tkv::IndexUpdate *dev_upd[2] = {nullptr, nullptr};
     int64_t upd_cap = 0;             // pairs per incremental upload
-    std::vector<int64_t> dirty;      // positions changed since the last upload
-    bool full = true;                // the next upload sends the whole table
     hipEvent_t ev[2] = {nullptr, nullptr};
     bool ev_used[2] = {false, false};
     int next = 0;
@@ -56,33 +48,6 @@ namespace {
 
 using tkv::IndexEntry;
 using tkv::IndexUpdate;
-using tkv::kEmpty;
-using tkv::kLive;
-using tkv::kTomb;
-
-// Position of `key`, or -1; *free_pos receives the first reusable position
-// met on the probe path (tombstone or empty), or -1 if none.
-int64_t probe(const kv_index *ix, uint64_t key, int64_t *free_pos) {
-    const uint64_t mask = (uint64_t)ix->cap - 1;
-    uint64_t pos = tkv::index_home(key, ix->log2cap);
-    int64_t first_free = -1;
-    for (int64_t n = 0; n < ix->cap; ++n) {
-        const IndexEntry &e = ix->host[pos];
-        if (e.state == kEmpty) {
-            if (first_free < 0) first_free = (int64_t)pos;
-            break;
-        }
-        if (e.state == kTomb) {
-            if (first_free < 0) first_free = (int64_t)pos;
-        } else if (e.key == key) {
-            if (free_pos) *free_pos = first_free;
-            return (int64_t)pos;
-        }
-        pos = (pos + 1) & mask;
-    }
-    if (free_pos) *free_pos = first_free;
-    return -1;
-}
 
 constexpr int kApplyThreads = 256;
 
@@ -94,40 +59,23 @@ __global__ __launch_bounds__(kApplyThreads) void index_apply_kernel(const IndexU
     if (pos >= 0 && pos < cap) table[pos] = upd[i].entry;
 }
 
-// Rebuild the table without tombstones.  It uses the spare table reserved at
-// creation, so no host memory is allocated here.
-void rehash(kv_index *ix) {
-    ix->full = true;
-    ix->dirty.clear();
-    ix->spare.swap(ix->host);
-    std::fill(ix->host.begin(), ix->host.end(), IndexEntry{0, -1, kEmpty});
-    ix->tombs = 0;
-    const uint64_t mask = (uint64_t)ix->cap - 1;
-    for (const IndexEntry &e : ix->spare) {
-        if (e.state != kLive) continue;
-        uint64_t pos = tkv::index_home(e.key, ix->log2cap);
-        while (ix->host[pos].state != kEmpty) pos = (pos + 1) & mask;
-        ix->host[pos] = e;
-    }
-}
-
 // Mirror the host mutations since the last upload into the device table.  An
 // incremental update stages its (position, entry) pairs in `upd_list`, a
-// device buffer of `upd_pairs` pairs; more changes than that send the whole
-// table image.
+// device buffer of `upd_pairs` pairs; more changes than that, or a rebuilt
+// table, send the whole table image.
 int upload_via(kv_index *ix, hipStream_t stream, IndexUpdate *upd_list, int64_t upd_pairs) {
+    tkv::IndexTable &t = ix->table;
     int prev = 0;
     if (hipGetDevice(&prev) != hipSuccess) return KV_EHIP;
     if (prev != ix->device && hipSetDevice(ix->device) != hipSuccess) return KV_EHIP;
     int rc = KV_OK;
     const int k = ix->next;
-    const size_t bytes = sizeof(IndexEntry) * (size_t)ix->cap;
+    const size_t bytes = sizeof(IndexEntry) * (size_t)t.cap;
     if (ix->ev_used[k] && hipEventSynchronize(ix->ev[k]) != hipSuccess) rc = KV_EHIP;
-    std::sort(ix->dirty.begin(), ix->dirty.end());
-    ix->dirty.erase(std::unique(ix->dirty.begin(), ix->dirty.end()), ix->dirty.end());
-    const int64_t n = (int64_t)ix->dirty.size();
-    if (rc == KV_OK && (ix->full || n > upd_pairs)) {
-        memcpy(ix->snap[k], ix->host.data(), bytes);
+    const std::vector<int64_t> &dirty = t.changes();
+    const int64_t n = (int64_t)dirty.size();
+    if (rc == KV_OK && (t.rebuilt || n > upd_pairs)) {
+        memcpy(ix->snap[k], t.entries.data(), bytes);
         if (hipMemcpyAsync(ix->dev, ix->snap[k], bytes, hipMemcpyHostToDevice, stream) != hipSuccess ||
             hipEventRecord(ix->ev[k], stream) != hipSuccess)
             rc = KV_EHIP;
@@ -135,14 +83,14 @@ int upload_via(kv_index *ix, hipStream_t stream, IndexUpdate *upd_list, int64_t 
             ix->ev_used[k] = true;
     } else if (rc == KV_OK && n > 0) {
         IndexUpdate *list = reinterpret_cast<IndexUpdate *>(ix->snap[k]);
-        for (int64_t i = 0; i < n; ++i) list[i] = IndexUpdate{ix->dirty[i], 0, ix->host[ix->dirty[i]]};
+        for (int64_t i = 0; i < n; ++i) list[i] = IndexUpdate{dirty[i], 0, t.entries[dirty[i]]};
         (void)hipGetLastError();
         if (hipMemcpyAsync(upd_list, list, sizeof(IndexUpdate) * (size_t)n, hipMemcpyHostToDevice, stream) !=
             hipSuccess) {
             rc = KV_EHIP;
         } else {
             hipLaunchKernelGGL(index_apply_kernel, dim3((unsigned)((n + kApplyThreads - 1) / kApplyThreads)),
-                               dim3(kApplyThreads), 0, stream, upd_list, n, ix->cap, ix->dev);
+                               dim3(kApplyThreads), 0, stream, upd_list, n, t.cap, ix->dev);
             if (hipGetLastError() != hipSuccess || hipEventRecord(ix->ev[k], stream) != hipSuccess)
                 rc = KV_EHIP;
             else
@@ -150,8 +98,8 @@ int upload_via(kv_index *ix, hipStream_t stream, IndexUpdate *upd_list, int64_t 
         }
     }
     if (rc == KV_OK) {
-        ix->full = false;
-        ix->dirty.clear();
+        t.rebuilt = false;
+        t.clear_changes();
     }
     ix->next = k ^ 1;
     if (prev != ix->device) (void)hipSetDevice(prev);
@@ -192,32 +140,6 @@ IndexUpdate *scratch_on(int device) {
     return g_scratch_ptr[device];
 }
 
-// Host half of an insert: mutate the authoritative table and record the
-// changed positions.  Returns KV_OK or KV_ENOSPC (the pairs before the
-// failing one stay inserted).
-int insert_host(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slots, int32_t n) {
-    int rc = KV_OK;
-    for (int32_t i = 0; i < n; ++i) {
-        int64_t free_pos = -1;
-        const int64_t at = probe(idx, h_keys[i], &free_pos);
-        if (at >= 0) {
-            idx->host[at].slot = h_slots[i];
-            idx->dirty.push_back(at);
-            continue;
-        }
-        if (idx->live >= idx->max_entries || free_pos < 0) {
-            rc = KV_ENOSPC;
-            break;
-        }
-        if (idx->host[free_pos].state == kTomb) --idx->tombs;
-        idx->host[free_pos] = IndexEntry{h_keys[i], h_slots[i], kLive};
-        idx->dirty.push_back(free_pos);
-        ++idx->live;
-        if ((idx->live + idx->tombs) * 4 > idx->cap * 3) rehash(idx);
-    }
-    return rc;
-}
-
 void release(kv_index *ix) {
     for (int k = 0; k < 2; ++k) {
         if (ix->ev[k]) {
@@ -235,7 +157,7 @@ void release(kv_index *ix) {
 
 namespace tkv {
 const IndexEntry *index_device_table(const kv_index *idx, int *log2cap) {
-    *log2cap = idx->log2cap;
+    *log2cap = idx->table.log2cap;
     return idx->dev;
 }
 }  // namespace tkv
@@ -247,18 +169,16 @@ int kv_index_create(int64_t max_entries, kv_index **out) {
     *out = nullptr;
     kv_index *ix = new (std::nothrow) kv_index();
     if (!ix) return KV_EINVAL;
-    ix->max_entries = max_entries;
-    ix->log2cap = 6;
-    while ((int64_t(1) << ix->log2cap) < 2 * max_entries) ++ix->log2cap;
-    ix->cap = int64_t(1) << ix->log2cap;
-    ix->host.assign(ix->cap, IndexEntry{0, -1, kEmpty});
-    ix->spare.assign(ix->cap, IndexEntry{0, -1, kEmpty});
     // changed positions between uploads: room for the largest allocation-free insert, and then some
-    ix->dirty.reserve(2 * (size_t)KV_INDEX_STATIC_MAX_PAIRS);
-    const size_t bytes = sizeof(IndexEntry) * (size_t)ix->cap;
+    if (!ix->table.init(max_entries, 2 * KV_INDEX_STATIC_MAX_PAIRS)) {
+        delete ix;
+        return KV_EINVAL;
+    }
+    const int64_t cap = ix->table.cap;
+    const size_t bytes = sizeof(IndexEntry) * (size_t)cap;
     // an incremental upload fits a snapshot buffer (cap entries = cap/2 pairs); past an eighth of the
     // table, or 65536 pairs, the whole image is sent instead
-    ix->upd_cap = std::min<int64_t>(ix->cap / 8, 65536);
+    ix->upd_cap = std::min<int64_t>(cap / 8, 65536);
     const size_t upd_bytes = sizeof(IndexUpdate) * (size_t)ix->upd_cap;
     if (hipGetDevice(&ix->device) != hipSuccess || hipMalloc((void **)&ix->dev, bytes) != hipSuccess ||
         hipMalloc((void **)&ix->dev_upd[0], upd_bytes) != hipSuccess ||
@@ -287,7 +207,7 @@ int kv_index_insert(kv_index *idx, const uint64_t *h_keys, const int32_t *h_slot
     if (!idx || n < 0 || (n > 0 && (!h_keys || !h_slots))) return KV_EINVAL;
     for (int32_t i = 0; i < n; ++i)
         if (h_slots[i] < 0) return KV_EINVAL;
-    const int rc = insert_host(idx, h_keys, h_slots, n);
+    const int rc = idx->table.insert(h_keys, h_slots, n);
     const int up = upload(idx, (hipStream_t)stream);
     return rc != KV_OK ? rc : up;
 }
@@ -304,36 +224,26 @@ int kv_index_insert_static(kv_index *idx, const uint64_t *h_keys, const int32_t 
     IndexUpdate *list = scratch_on(idx->device);
     if (prev != idx->device) (void)hipSetDevice(prev);
     if (!list) return KV_EHIP;
-    const int rc = insert_host(idx, h_keys, h_slots, n);
+    const int rc = idx->table.insert(h_keys, h_slots, n);
     const int up = upload_via(idx, (hipStream_t)stream, list, std::min<int64_t>(idx->upd_cap, kStaticPairs));
     return rc != KV_OK ? rc : up;
 }
 
 int kv_index_erase(kv_index *idx, const uint64_t *h_keys, int32_t n, void *stream) {
     if (!idx || n < 0 || (n > 0 && !h_keys)) return KV_EINVAL;
-    for (int32_t i = 0; i < n; ++i) {
-        const int64_t at = probe(idx, h_keys[i], nullptr);
-        if (at < 0) continue;
-        idx->host[at].state = kTomb;
-        idx->host[at].slot = -1;
-        idx->dirty.push_back(at);
-        --idx->live;
-        ++idx->tombs;
-    }
-    if ((idx->live + idx->tombs) * 4 > idx->cap * 3) rehash(idx);
+    idx->table.erase(h_keys, n);
     return upload(idx, (hipStream_t)stream);
 }
 
 int kv_index_size(const kv_index *idx, int64_t *out) {
     if (!idx || !out) return KV_EINVAL;
-    *out = idx->live;
+    *out = idx->table.live;
     return KV_OK;
 }
 
 int kv_index_find(const kv_index *idx, uint64_t key, int32_t *slot_out) {
     if (!idx || !slot_out) return KV_EINVAL;
-    const int64_t at = probe(idx, key, nullptr);
-    *slot_out = at >= 0 ? idx->host[at].slot : -1;
+    *slot_out = idx->table.find(key);
     return KV_OK;
 }
 

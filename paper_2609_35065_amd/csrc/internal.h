@@ -5,27 +5,10 @@
 #include <stdint.h>
 
 #include "host.h"
+#include "index_table.h"
 #include "tempokv.h"
 
 namespace tkv {
-
-// Device-table entry of the staged-chunk index: 16 bytes, read by one
-// dwordx4 load in the probe loop.
-struct alignas(16) IndexEntry {
-    uint64_t key;
-    int32_t slot;
-    int32_t state;   // kEmpty, kLive or kTomb
-};
-constexpr int32_t kEmpty = 0;
-constexpr int32_t kLive = 1;
-constexpr int32_t kTomb = 2;
-
-// Home position of a key in a table of 2^log2cap entries (Fibonacci
-// hashing: the high bits of key * 2^64/phi), so that any key set, including
-// small or sequential keys, spreads over the table.
-__host__ __device__ inline uint64_t index_home(uint64_t key, int log2cap) {
-    return (key * 0x9E3779B97F4A7C15ull) >> (64 - log2cap);
-}
 
 // Everything the copy kernels need, passed by value in the kernel-argument
 // segment so that the per-layer base pointers are read with scalar loads and

@@ -33,7 +33,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_strerror():
     assert "gfx950" in kv.kv_version()
-    for code in [0, -1, -2, -3, -4, -5, -6]:
+    for code in [0, -1, -2, -3, -4, -5, -6, -7]:
         assert kv.strerror(code) and kv.strerror(code) != "unknown status"
     assert kv.strerror(-99) == "unknown status"
 
@@ -66,7 +66,7 @@ def test_batched_commit_rule_matches_oracle_elementwise(seed):
     assert got.tolist() == exp
     assert kv.KV_EINVAL in exp and kv.KV_COMMIT in exp           # invalid elements do not stop the batch
     assert kv.kv_commit_should_stage_n([], [], 0, [], [], 0, []).size == 0
-    L = kv.lib()
+    L = kv.host_lib()
     assert L.kv_commit_should_stage_n(-1, None, None, 0, None, None, 0, None, None) == kv.KV_EINVAL
     assert L.kv_commit_should_stage_n(3, None, None, 0, None, None, 0, None, None) == kv.KV_EINVAL
     assert L.kv_commit_should_stage_n(0, None, None, 0, None, None, 0, None, None) == kv.KV_OK
@@ -204,7 +204,7 @@ def test_group_jobs_by_slot_is_a_stable_sort(seed):
     got = kv.kv_group_jobs_by_slot(jobs)
     want = jobs[np.argsort(jobs[:, 0], kind="stable")]
     assert np.array_equal(got, want)
-    assert kv.lib().kv_group_jobs_by_slot(None, -1) == kv.KV_EINVAL
+    assert kv.host_lib().kv_group_jobs_by_slot(None, -1) == kv.KV_EINVAL
 
 
 def test_stage_calls_check_arguments_before_any_copy():
@@ -266,7 +266,7 @@ def test_retrieve_plan_rules():
     rng = np.random.default_rng(3)
     sizes = rng.integers(1, 9, 200)
     assert P(lo32, _jobs(np.repeat(np.arange(200), sizes))) == kv.KV_RETRIEVE_UNIT    # irregular groups
-    L = kv.lib()
+    L = kv.host_lib()
     assert L.kv_retrieve_plan(None, None, 0) == kv.KV_EINVAL
     assert L.kv_retrieve_plan(ct.byref(lo32), None, 3) == kv.KV_EINVAL
     assert L.kv_retrieve_plan(ct.byref(lo32), None, -1) == kv.KV_EINVAL
