@@ -8,8 +8,9 @@ every byte of the GPU's layer (written blocks, untouched blocks) and of every
 staging slot's part for that layer (stored, read and untouched slots) is
 compared.  Only one layer's buffers per worker are held on the host.
 
-Sampled comparison for every configuration: buffers of 20-170 GiB cannot be
-held twice on the host, so:
+Every other configuration: its first and last layer compared in full the
+same way, and every layer on samples (buffers of 20-170 GiB cannot be held
+twice on the host):
   * hash, lookup and the job lists are compared in full with the oracle;
   * copies are checked on sampled segments: for a sampled paged block the
     oracle says (one by one) which staged segment, if any, lands there, and
@@ -43,7 +44,7 @@ def _seg_view(w, layer_tensor, kv, blk):
     return layer_tensor[off:off + seg], off
 
 
-def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy", force_kind=None):
+def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy", force_kind=None, complete_edges=False):
     w = W.make(name)
     print(f"[fullsize] {name}: {w.num_reqs} reqs, pool {w.pool_bytes() / 2**30:.1f} GiB, "
           f"staging {w.staged_bytes() / 2**30:.1f} GiB, lower tier {lower_tier}, retrieve {force_kind}", flush=True)
@@ -122,6 +123,10 @@ def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy", force_k
                 _, poff = _seg_view(w, g.layers[l], kvp, blk)
                 exp = W.kv_bytes_np(POOL_TAG + l, w.seed, poff, seg)
                 assert np.array_equal(got, exp), (name, "gather", s, l, kvp, i)
+    if complete_edges:
+        # every byte of the first and the last layer: pool and every staging slot
+        n = _check_layers(w, g, o, retr, store, sorted({0, L - 1}), 2)
+        print(f"[fullsize] {name}: layers 0 and {L - 1} compared in full ({n / 2**30:.1f} GiB)", flush=True)
     del g
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
@@ -136,7 +141,7 @@ FULL = ["l32-64x4096", "l32-lognormal-p25", "l32-lognormal-p50", "l32-lognormal-
 
 @pytest.mark.parametrize("name", FULL)
 def test_full_size_sampled(name):
-    check_full_size(name)
+    check_full_size(name, complete_edges=True)
 
 
 @pytest.mark.parametrize("name", ["l32-1x65536-host", "l32-1024x1024-cap100-host"])
@@ -172,12 +177,44 @@ def _layer_check(w, g, o, retr, store, l, bufs):
     oracle.retrieve_scatter_layer(o.layout, exp_stg, exp_pool, w.block_tables, retr)
     oracle.store_gather_layer(o.layout, exp_stg, exp_pool, w.block_tables, store)
     got_pool.copy_(g.layers[l])
-    got_stg.copy_(g.staging.view(S, L, part)[:, l, :].reshape(-1))
+    got_stg.copy_(g.staging_view().view(S, L, part)[:, l, :].reshape(-1))
     ok_pool = np.array_equal(got_pool.numpy(), exp_pool)
     ok_stg = np.array_equal(got_stg.numpy(), exp_stg)
     assert ok_pool, f"layer {l}: paged tensor differs"
     assert ok_stg, f"layer {l}: staging differs"
     return exp_pool.size + exp_stg.size
+
+
+def _check_layers(w, g, o, retr, store, layers, workers):
+    """_layer_check over `layers`, `workers` layers at a time; returns the bytes compared."""
+    L, S = w.shape.num_layers, w.num_slots
+    part = oracle.layer_part_bytes(o.layout)
+    nw = max(1, min(workers, (os.cpu_count() or 4), len(layers)))
+    pools = [(np.empty(w.layer_bytes(), np.uint8), np.empty(S * part, np.uint8),
+              torch.from_numpy(np.empty(w.layer_bytes(), np.uint8)),
+              torch.from_numpy(np.empty(S * part, np.uint8))) for _ in range(nw)]
+    free = list(range(nw))
+    total = 0
+
+    def one(l, k):
+        with torch.cuda.stream(torch.cuda.Stream()):
+            n = _layer_check(w, g, o, retr, store, l, pools[k])
+            torch.cuda.current_stream().synchronize()
+        return n
+
+    with cf.ThreadPoolExecutor(nw) as ex:
+        pending = {}
+        for l in layers:
+            if not free:
+                done, _ = cf.wait(pending, return_when=cf.FIRST_COMPLETED)
+                for f in done:
+                    total += f.result()
+                    free.append(pending.pop(f))
+            k = free.pop()
+            pending[ex.submit(one, l, k)] = k
+        for f in cf.as_completed(pending):
+            total += f.result()
+    return total
 
 
 def check_full_size_complete(name, workers=8):
@@ -195,35 +232,9 @@ def check_full_size_complete(name, workers=8):
     assert np.array_equal(g.last_retrieve, so["retrieve"]) and np.array_equal(g.last_store, so["store"])
     assert sg.num_retrieve > 0 and sg.num_store > 0
     retr, store = so["retrieve"], so["store"]
-    L, S = w.shape.num_layers, w.num_slots
-    part = oracle.layer_part_bytes(o.layout)
-    nw = max(1, min(workers, (os.cpu_count() or 4), L))
-    pools = [(np.empty(w.layer_bytes(), np.uint8), np.empty(S * part, np.uint8),
-              torch.from_numpy(np.empty(w.layer_bytes(), np.uint8)),
-              torch.from_numpy(np.empty(S * part, np.uint8))) for _ in range(nw)]
-    free = list(range(nw))
-    total = 0
-
-    def one(l, k):
-        with torch.cuda.stream(torch.cuda.Stream()):
-            n = _layer_check(w, g, o, retr, store, l, pools[k])
-            torch.cuda.current_stream().synchronize()
-        return n
-
-    with cf.ThreadPoolExecutor(nw) as ex:
-        pending = {}
-        for l in range(L):
-            if not free:
-                done, _ = cf.wait(pending, return_when=cf.FIRST_COMPLETED)
-                for f in done:
-                    total += f.result()
-                    free.append(pending.pop(f))
-            k = free.pop()
-            pending[ex.submit(one, l, k)] = k
-        for f in cf.as_completed(pending):
-            total += f.result()
+    total = _check_layers(w, g, o, retr, store, range(w.shape.num_layers), workers)
     print(f"[complete] {name}: {total / 2**30:.1f} GiB compared in {time.perf_counter() - t0:.0f} s", flush=True)
-    del g, pools
+    del g
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
 
@@ -236,4 +247,4 @@ def test_full_size_every_byte(name):
 @pytest.mark.parametrize("name", ["l32-1024x1024-cap50-host", "l32-1024x1024-cap100-host"])
 def test_full_size_sampled_zero_copy_from_host(name):
     # the capacity sweep's host-staged points in the bench's default zero-copy mode
-    check_full_size(name, lower_tier="zero-copy")
+    check_full_size(name, lower_tier="zero-copy", complete_edges=True)
