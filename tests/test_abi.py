@@ -279,3 +279,14 @@ def test_retrieve_as_rejects_unknown_kinds():
     for kind in (-1, 4, 99):
         assert L.kv_retrieve_scatter_as(kind, ct.byref(lo), 0x10000, layers, 0x10000, 10, 2, 0x10000, 1,
                                         None) == kv.KV_EINVAL
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_chunk_keys_match_oracle(seed):
+    bh, blk_off, chunk_off, bpc, cs, hit = _lookup_case(seed)
+    got = kv.kv_chunk_keys(bh, blk_off, bpc, chunk_off)
+    assert np.array_equal(got, oracle.chunk_keys(bh, blk_off, bpc))
+    with pytest.raises(kv.KvError):          # offsets that do not match blocks_per_chunk
+        bad = chunk_off.copy()
+        bad[-1] += 1
+        kv.kv_chunk_keys(bh, blk_off, bpc, bad)
