@@ -286,7 +286,8 @@ def test_chunk_keys_match_oracle(seed):
     bh, blk_off, chunk_off, bpc, cs, hit = _lookup_case(seed)
     got = kv.kv_chunk_keys(bh, blk_off, bpc, chunk_off)
     assert np.array_equal(got, oracle.chunk_keys(bh, blk_off, bpc))
-    with pytest.raises(kv.KvError):          # offsets that do not match blocks_per_chunk
-        bad = chunk_off.copy()
-        bad[-1] += 1
-        kv.kv_chunk_keys(bh, blk_off, bpc, bad)
+    if blk_off.size > 1:
+        with pytest.raises(kv.KvError):      # offsets that do not match blocks_per_chunk
+            bad = chunk_off.copy()
+            bad[-1] += 1
+            kv.kv_chunk_keys(bh, blk_off, bpc, bad)
