@@ -42,6 +42,9 @@ METRIC = "paged-KV scatter/gather GB/s (% of HBM peak); prefix-hash Mtok/s"
 HBM_PEAK_GBS = 8000.0
 STG_TAG, POOL_TAG = 1, 1000
 PROFILES = os.path.join(ROOT, "profiles")
+# the same-pool ceiling: launches of each of its two measurements (writes alone, writes with the unique reads)
+CEILING_REPS = 5
+CEILING_LAUNCHES = 2 * CEILING_REPS
 
 
 def _src_digest() -> str:
@@ -168,6 +171,10 @@ def profile_commands(workload: str, out: str) -> list:
         cmds.append((name, f"rocprofv3 --pmc {ctrs} --kernel-include-regex tkv -f csv -d {out}/{name} -o c -- {b3}"))
     for name, ctr in (("cal_fetch", "FETCH_SIZE"), ("cal_write", "WRITE_SIZE")):
         cmds.append((name, f"rocprofv3 --pmc {ctr} -f csv -d {out}/{name} -o c -- python3 bench.py --calib-copy"))
+    # the retrieve's same-pool ceiling alone (every kernel counted: its reads are torch reductions)
+    cc = f"python3 bench.py --warmup 1 --no-fill --ceiling-only --workload {workload}"
+    for name, ctr in (("ceil_fetch", "FETCH_SIZE"), ("ceil_write", "WRITE_SIZE")):
+        cmds.append((name, f"rocprofv3 --pmc {ctr} -f csv -d {out}/{name} -o c -- {cc}"))
     return cmds
 
 
@@ -216,19 +223,24 @@ def _counter_medians(directory: str):
     return {k: statistics.median(v) for k, v in agg.items()}
 
 
+def _calibration_scales(cal_dir: str):
+    """FETCH_SIZE and WRITE_SIZE scale factors from the calibration copy (4 GiB each way)."""
+    w_cal = 4 << 30
+    cf = [v for (k, c), v in _counter_medians(os.path.join(cal_dir, "cal_fetch")).items() if "copy_generic" in k]
+    cw = [v for (k, c), v in _counter_medians(os.path.join(cal_dir, "cal_write")).items() if "copy_generic" in k]
+    return w_cal / 1024 / cf[0], w_cal / 1024 / cw[0], cf[0], cw[0]
+
+
 def summarize_traffic(directory: str, workload: str, calibration: str = None) -> list:
     """profiles/traffic_*_{workload}.txt: FETCH_SIZE and WRITE_SIZE per launch
     of the store and of the retrieve variant the timed steps ran, scaled by
     what the same counters read for the calibration copy of known size."""
-    w_cal = 4 << 30
     cal_dir = calibration or directory
     cmds = dict(profile_commands(workload, "gpurun_out/prof_" + workload))
     cal_wl = os.path.basename(os.path.normpath(cal_dir))[len("prof_"):] or workload
     cmds.update({k: v for k, v in profile_commands(cal_wl, "gpurun_out/prof_" + cal_wl) if k.startswith("cal_")})
     fe, wr = _counter_medians(os.path.join(directory, "pmc_fetch")), _counter_medians(os.path.join(directory, "pmc_write"))
-    cf = [v for (k, c), v in _counter_medians(os.path.join(cal_dir, "cal_fetch")).items() if "copy_generic" in k]
-    cw = [v for (k, c), v in _counter_medians(os.path.join(cal_dir, "cal_write")).items() if "copy_generic" in k]
-    f_fetch, f_write = w_cal / 1024 / cf[0], w_cal / 1024 / cw[0]
+    f_fetch, f_write, cf, cw = _calibration_scales(cal_dir)
     d = _bench_json(os.path.join(directory, "pmc_fetch.log"))
     variant = d["config"]["retrieve_variant"]
     import workloads as W
@@ -256,7 +268,7 @@ def summarize_traffic(directory: str, workload: str, calibration: str = None) ->
                f"timed_variant={variant}" + ("" if kern == "kv_copy_store" or kern.endswith(variant) else
                                               " (this variant ran in the retrieve tuning before the timed steps)"),
                f"fetch_kib_per_dispatch={fk:.1f}", f"write_kib_per_dispatch={wk:.1f}",
-               f"calibration_fetch_kib={cf[0]:.1f}", f"calibration_write_kib={cw[0]:.1f}",
+               f"calibration_fetch_kib={cf:.1f}", f"calibration_write_kib={cw:.1f}",
                f"fetch_scale={f_fetch:.4f}", f"write_scale={f_write:.4f}",
                f"hbm_read_bytes_per_launch={fk * f_fetch * 1024:.0f}",
                f"hbm_write_bytes_per_launch={wk * f_write * 1024:.0f}",
@@ -265,6 +277,69 @@ def summarize_traffic(directory: str, workload: str, calibration: str = None) ->
         open(path, "w").write("\n".join(txt) + "\n")
         out.append(path)
     return out
+
+
+def summarize_ceiling(directory: str, workload: str, calibration: str = None):
+    """profiles/traffic_retrieve_ceiling_{workload}.txt: HBM bytes of the
+    retrieve's same-pool ceiling, from a --ceiling-only run under FETCH_SIZE
+    and one under WRITE_SIZE.  The ceiling's retrieve launches (every job
+    reading one staged chunk) are the last CEILING_LAUNCHES launches of the
+    retrieve kernel in the run; its reads of the unique staged chunks are the
+    torch reduction kernels (CEILING_LAUNCHES passes over the chunks).
+    Returns the path, or None when the run measured no ceiling."""
+    import statistics
+    from collections import defaultdict
+    cal_dir = calibration or directory
+    d = _bench_json(os.path.join(directory, "ceil_fetch.log"))
+    if not d or not d.get("ceiling"):
+        return None
+    n = int(d["ceiling_launches"])
+    variant = d["config"]["retrieve_variant"]
+    import workloads as W
+    sym = _symbol(variant, W.make(workload))
+    f_fetch, f_write, cf, cw = _calibration_scales(cal_dir)
+    res = {}
+    for kind, ctr, scale in (("ceil_fetch", "FETCH_SIZE", f_fetch), ("ceil_write", "WRITE_SIZE", f_write)):
+        rows = [r for r in _csv_rows(os.path.join(directory, kind), "_counter_collection.csv")
+                if r["Counter_Name"] == ctr]
+        mine = sorted((int(r["Dispatch_Id"]), float(r["Counter_Value"])) for r in rows
+                      if _short_symbol(r["Kernel_Name"]) == sym)
+        if len(mine) < n:
+            raise ValueError(f"{kind}: {len(mine)} launches of {sym}, expected at least {n}")
+        per_reader = defaultdict(float)
+        for r in rows:
+            if "reduce_kernel" in r["Kernel_Name"]:
+                per_reader[_short_symbol(r["Kernel_Name"]).split("<")[0]] += float(r["Counter_Value"])
+        res[kind] = (statistics.median(v for _, v in mine[-n:]) * scale * 1024,
+                     sum(per_reader.values()) / n * scale * 1024, len(mine))
+    c = d["ceiling"]
+    cmds = dict(profile_commands(workload, "gpurun_out/prof_" + workload))
+    cal_wl = os.path.basename(os.path.normpath(cal_dir))[len("prof_"):] or workload
+    cmds.update({k: v for k, v in profile_commands(cal_wl, "gpurun_out/prof_" + cal_wl) if k.startswith("cal_")})
+    wo_read, rd_read, nl = res["ceil_fetch"]
+    wo_write, rd_write, _ = res["ceil_write"]
+    txt = [f"# HBM traffic of the retrieve's same-pool ceiling, workload {workload}",
+           "# Made by `python bench.py --summarize-ceiling` from these runs (repository root, one MI355X):",
+           *[f"#   {cmds[k]}" for k in ("ceil_fetch", "ceil_write", "cal_fetch", "cal_write")],
+           "# The ceiling re-runs the retrieve's own jobs, variant and destination blocks with every job reading",
+           "# one staged chunk (its scattered writes alone), and reads the retrieve's unique staged chunks with",
+           "# torch reductions, alone and concurrently with those writes.  Counters: the median over the last",
+           f"# {n} launches of the retrieve kernel (the ceiling's; the warm-up pass and the tuning launch it",
+           "# before them) and the reductions' sum divided by the number of read passes, scaled by the calibration",
+           "# copy's readings as in the traffic files of the copy kernels.",
+           f"workload={workload}", f"symbol={sym}", f"retrieve_variant={variant}",
+           f"retrieve_launches_in_run={nl}", f"ceiling_launches={n}",
+           f"fetch_scale={f_fetch:.4f}", f"write_scale={f_write:.4f}",
+           f"writes_only_hbm_read_bytes_per_launch={wo_read:.0f}",
+           f"writes_only_hbm_write_bytes_per_launch={wo_write:.0f}",
+           f"unique_read_hbm_read_bytes_per_pass={rd_read:.0f}",
+           f"unique_read_hbm_write_bytes_per_pass={rd_write:.0f}",
+           f"ceiling_traffic_bytes={wo_read + wo_write + rd_read + rd_write:.0f}"]
+    if isinstance(c, dict) and "writes_with_unique_read" in c:
+        txt.append(f"# timings of this run are not quoted: counter collection serialises the two streams")
+    path = os.path.join(PROFILES, f"traffic_retrieve_ceiling_{workload}.txt")
+    open(path, "w").write("\n".join(txt) + "\n")
+    return path
 
 
 def summarize_counters(directory: str, workload: str) -> str:
@@ -359,7 +434,7 @@ def _cpu_model() -> str:
     return "unknown"
 
 
-def _retrieve_write_bound(path, torch, reps: int = 5):
+def _retrieve_write_bound(path, torch, reps: int = CEILING_REPS):
     """The timed retrieve's writes on their own: the same jobs, variant and
     destination blocks, but every job reading one staged chunk (which stays in
     L2), so HBM sees only the scattered 32 KiB writes.  Its time bounds the
@@ -390,7 +465,7 @@ def _retrieve_write_bound(path, torch, reps: int = 5):
     written = n * w.shape.slot_bytes
     out = {"ms": round(t, 4), "GB/s_written": round(written / (t * 1e-3) / 1e9, 1),
            "what": "the timed retrieve's jobs and variant with every job reading one staged chunk: its "
-                   "scattered writes alone (median of 5)"}
+                   f"scattered writes alone (median of {reps})"}
     # The same writes with the unique staged chunks read from HBM at the same time, on a second stream:
     # the retrieve's algorithmic bytes (unique reads + writes) with no kernel of ours reading them.  The
     # reads are torch reductions over the contiguous runs of the chunks' slots.
@@ -435,7 +510,7 @@ def _retrieve_write_bound(path, torch, reps: int = 5):
                           "what": "the retrieve's unique staged chunks read once (torch reductions), idle GPU"}
     out["writes_with_unique_read"] = {
         "ms": round(t_mx, 4), "GB/s_alg": round((uniq + written) / (t_mx * 1e-3) / 1e9, 1),
-        "what": "the scattered writes alone and the unique reads, concurrently on two streams (median of 5): "
+        "what": f"the scattered writes alone and the unique reads, concurrently on two streams (median of {reps}): "
                 "the retrieve's algorithmic bytes on this pool without the retrieve's own reads"}
     return out
 
@@ -667,6 +742,9 @@ def main() -> int:
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the same-pool ceilings and practical-peak copies after the timed steps (kernel "
                          "traces: every launch of a copy kernel is then a step's, a tuning or an idle-GPU pass's)")
+    ap.add_argument("--ceiling-only", action="store_true",
+                    help="after the warm-up (and the retrieve tuning) run only the retrieve's same-pool ceiling "
+                         "launches, print them and exit (the counter passes behind that ceiling)")
     ap.add_argument("--profile-commands", metavar="OUTDIR",
                     help="print the rocprofv3 runs behind the profiles of --workload, writing under OUTDIR "
                          "(name<TAB>command per line), and exit")
@@ -676,6 +754,9 @@ def main() -> int:
     ap.add_argument("--summarize-traffic", metavar="DIR",
                     help="write profiles/traffic_*_<workload>.txt from the pmc_fetch, pmc_write, cal_fetch and "
                          "cal_write runs under DIR and exit")
+    ap.add_argument("--summarize-ceiling", metavar="DIR",
+                    help="write profiles/traffic_retrieve_ceiling_<workload>.txt from the ceil_fetch and ceil_write "
+                         "runs under DIR (calibration from --calibration or DIR) and exit")
     ap.add_argument("--summarize-counters", metavar="DIR",
                     help="write profiles/counters_<workload>.md from the sq, tcc, tlb and occ runs under DIR and exit")
     ap.add_argument("--command", default="", help="the command a --summarize-trace run was made with")
@@ -695,6 +776,9 @@ def main() -> int:
         return 0
     if args.summarize_counters:
         print(summarize_counters(args.summarize_counters, args.workload))
+        return 0
+    if args.summarize_ceiling:
+        print(summarize_ceiling(args.summarize_ceiling, args.workload, args.calibration))
         return 0
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -749,6 +833,13 @@ def main() -> int:
     print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
     # pick the retrieve variant for this pool by timing (outside the timed steps)
     tuning = path.tune_retrieve() if args.warmup and not args.no_tune else {}
+    if args.ceiling_only:
+        # the last CEILING_LAUNCHES launches of the retrieve kernel in this process are the ceiling's
+        print(json.dumps({"workload": w.name, "config": {"retrieve_variant": RETRIEVE_KIND_NAMES.get(path.retrieve_kind),
+                                                        "retrieve_tuning_ms": tuning},
+                          "ceiling_launches": CEILING_LAUNCHES,
+                          "ceiling": _retrieve_write_bound(path, torch, reps=CEILING_REPS)}))
+        return 0
 
     timers: dict = {}
     torch.cuda.synchronize()

@@ -93,3 +93,41 @@ def test_traffic_summary_scales_by_the_calibration(tmp_path, monkeypatch):
     # the bench line reads them back only while the copy sources are unchanged
     assert bench._load_traffic("kv_copy_retrieve", "l32-64x4096", "quad") == (20 + 50) * 1024
     assert bench._load_traffic("kv_copy_retrieve", "l32-64x4096", "pair") is None
+
+
+def test_ceiling_summary_takes_the_ceiling_launches(tmp_path, monkeypatch):
+    monkeypatch.setattr(bench, "PROFILES", str(tmp_path))
+    d = tmp_path / "prof"
+    quad = "tkv::(anonymous namespace)::retrieve_quad_kernel<8>(tkv::CopyParams)"
+    red = "void at::native::reduce_kernel<512, 1>(at::native::ReduceOp<long>)"
+    cal = "tkv::(anonymous namespace)::copy_generic_kernel<true>(tkv::CopyParams)"
+    n = bench.CEILING_LAUNCHES
+
+    def rows(ctr, real, ceil, reader):
+        out, i = [], 0
+        for v in [real] * 5 + [ceil] * n:          # warm-up and tuning launches first, then the ceiling's
+            i += 1
+            out.append({"Dispatch_Id": str(i), "Kernel_Name": quad, "Counter_Name": ctr, "Counter_Value": str(v)})
+        for _ in range(n):                          # one reduction per read pass
+            i += 1
+            out.append({"Dispatch_Id": str(i), "Kernel_Name": red, "Counter_Name": ctr, "Counter_Value": str(reader)})
+        return out
+
+    _write_csv(str(d / "ceil_fetch" / "c_counter_collection.csv"), rows("FETCH_SIZE", 1000, 10, 100))
+    _write_csv(str(d / "ceil_write" / "c_counter_collection.csv"), rows("WRITE_SIZE", 4000, 4000, 0))
+    row = lambda c, v: {"Dispatch_Id": "1", "Kernel_Name": cal, "Counter_Name": c, "Counter_Value": str(v)}
+    _write_csv(str(d / "cal_fetch" / "c_counter_collection.csv"), [row("FETCH_SIZE", (4 << 20) / 2)])
+    _write_csv(str(d / "cal_write" / "c_counter_collection.csv"), [row("WRITE_SIZE", 4 << 20)])
+    (d / "ceil_fetch.log").write_text('{"config": {"retrieve_variant": "quad"}, "ceiling_launches": %d, '
+                                      '"ceiling": {"ms": 3.2}}\n' % n)
+    path = bench.summarize_ceiling(str(d), "l32-64x4096")
+    kv = dict(l.strip().split("=", 1) for l in open(path) if "=" in l and not l.startswith("#"))
+    assert kv["symbol"] == "retrieve_quad_kernel<8>"
+    assert float(kv["writes_only_hbm_read_bytes_per_launch"]) == 10 * 2 * 1024      # FETCH_SIZE scale 2
+    assert float(kv["writes_only_hbm_write_bytes_per_launch"]) == 4000 * 1024
+    assert float(kv["unique_read_hbm_read_bytes_per_pass"]) == 100 * 2 * 1024
+    assert int(kv["retrieve_launches_in_run"]) == 5 + n
+    # no ceiling measured (streaming retrieve, or staged chunks in host memory): no file
+    (d / "ceil_fetch.log").write_text('{"config": {"retrieve_variant": "stream"}, "ceiling_launches": %d, '
+                                      '"ceiling": null}\n' % n)
+    assert bench.summarize_ceiling(str(d), "l32-64x4096") is None
