@@ -1,24 +1,26 @@
 """GPU parity at the full workload sizes, in the launch configuration the
 benchmark times.
 
-Complete comparison, one layer at a time (the 32- and 80-layer batches): for
-every layer the oracle's one-layer walks rebuild the expected paged tensor and
-the expected staging contents from the input formula and the job lists, and
-every byte of the GPU's layer (written blocks, untouched blocks) and of every
-staging slot's part for that layer (stored, read and untouched slots) is
-compared.  Only one layer's buffers per worker are held on the host.
-
-Every other configuration: its first and last layer compared in full the
-same way, and every layer on samples (buffers of 20-170 GiB cannot be held
-twice on the host):
+Every configuration:
   * hash, lookup and the job lists are compared in full with the oracle;
   * copies are checked on sampled segments: for a sampled paged block the
     oracle says (one by one) which staged segment, if any, lands there, and
     the expected bytes are recomputed from the input generator's formula; the
     same for sampled staging segments written by the store gather.  Samples
     cover every layer, both planes, the first and last jobs, and blocks that
-    no job touches (which must keep their original bytes)."""
+    no job touches (which must keep their original bytes);
+  * complete comparison, one layer at a time: for a layer the oracle's
+    one-layer walks rebuild the expected paged tensor and the expected
+    staging contents from the input formula and the job lists, and every
+    byte of the GPU's layer (written blocks, untouched blocks) and of every
+    staging slot's part for that layer (stored, read and untouched slots) is
+    compared, with only one layer's buffers per worker held on the host
+    (buffers of 20-170 GiB cannot be held twice).  Every layer for one
+    configuration of each workload family (EVERY_BYTE; all of them with
+    TEMPOKV_EVERY_BYTE_ALL=1, about 1.7 TiB and six and a half minutes), the first and the
+    last layer for the others."""
 import concurrent.futures as cf
+import ctypes
 import os
 import time
 
@@ -44,7 +46,9 @@ def _seg_view(w, layer_tensor, kv, blk):
     return layer_tensor[off:off + seg], off
 
 
-def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy", force_kind=None, complete_edges=False):
+def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy", force_kind=None, layers=None):
+    """layers: None (samples only), "edges" (also the first and the last layer
+    in full) or "all" (also every layer in full)."""
     w = W.make(name)
     print(f"[fullsize] {name}: {w.num_reqs} reqs, pool {w.pool_bytes() / 2**30:.1f} GiB, "
           f"staging {w.staged_bytes() / 2**30:.1f} GiB, lower tier {lower_tier}, retrieve {force_kind}", flush=True)
@@ -123,10 +127,13 @@ def check_full_size(name, n_samples=600, seed=0, lower_tier="zero-copy", force_k
                 _, poff = _seg_view(w, g.layers[l], kvp, blk)
                 exp = W.kv_bytes_np(POOL_TAG + l, w.seed, poff, seg)
                 assert np.array_equal(got, exp), (name, "gather", s, l, kvp, i)
-    if complete_edges:
-        # every byte of the first and the last layer: pool and every staging slot
-        n = _check_layers(w, g, o, retr, store, sorted({0, L - 1}), 2)
-        print(f"[fullsize] {name}: layers 0 and {L - 1} compared in full ({n / 2**30:.1f} GiB)", flush=True)
+    if layers is not None:
+        # every byte of the chosen layers: pool and every staging slot
+        t0 = time.perf_counter()
+        sel = range(L) if layers == "all" else sorted({0, L - 1})
+        n = _check_layers(w, g, o, retr, store, sel, 8 if layers == "all" else 2)
+        print(f"[fullsize] {name}: {len(sel)} of {L} layers compared in full ({n / 2**30:.1f} GiB, "
+              f"{time.perf_counter() - t0:.0f} s)", flush=True)
     del g
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
@@ -139,9 +146,21 @@ FULL = ["l32-64x4096", "l32-lognormal-p25", "l32-lognormal-p50", "l32-lognormal-
         "l32-64x4096-pad4096"]
 
 
+HOST_ZERO_COPY = ["l32-1024x1024-cap50-host", "l32-1024x1024-cap100-host", "l32-1x65536-host"]
+# every byte of every layer: one configuration of each workload family in every run
+EVERY_BYTE = ["l32-64x4096", "l48-64x4096", "l80-32x8192", "l32-lognormal-p50", "l32-1024x1024-cap25-hbm",
+              "l32-1x65536", "l48-1x65536", "l32-1x65536-host"]
+if os.environ.get("TEMPOKV_EVERY_BYTE_ALL"):
+    EVERY_BYTE = FULL + HOST_ZERO_COPY
+
+
+def _layers(name):
+    return "all" if name in EVERY_BYTE else "edges"
+
+
 @pytest.mark.parametrize("name", FULL)
-def test_full_size_sampled(name):
-    check_full_size(name, complete_edges=True)
+def test_full_size(name):
+    check_full_size(name, layers=_layers(name))
 
 
 @pytest.mark.parametrize("name", ["l32-1x65536-host", "l32-1024x1024-cap100-host"])
@@ -154,14 +173,31 @@ def test_full_size_sampled_pipelined_from_host(name):
 
 @pytest.mark.parametrize("name", ["l32-64x4096", "l48-64x4096", "l32-lognormal-p75", "l32-1024x1024-cap25-hbm",
                                   "l32-64x4096-pad4096"])
-def test_full_size_sampled_quad_retrieve(name):
-    # the four-job-window retrieve, which tune_retrieve may choose for a pool
-    check_full_size(name, force_kind=kv.KV_RETRIEVE_QUAD)
+def test_full_size_quad_retrieve(name):
+    # the four-job-window retrieve, which tune_retrieve may choose for a pool (on the 32-layer batch it
+    # usually does, so there it is compared in full)
+    check_full_size(name, force_kind=kv.KV_RETRIEVE_QUAD, layers="all" if name == "l32-64x4096" or os.environ.get("TEMPOKV_EVERY_BYTE_ALL") else "edges")
 
 
 # ---------------------------------------------------------------------------
 # complete comparison, streamed one layer at a time
 # ---------------------------------------------------------------------------
+
+_libc = ctypes.CDLL(None)
+_libc.memcmp.restype = ctypes.c_int
+_libc.memcmp.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t]
+
+
+def _same(got: np.ndarray, exp: np.ndarray) -> bool:
+    """Byte equality of two contiguous uint8 arrays (memcmp: no temporary the
+    size of the buffers, and the GIL is released while it runs)."""
+    assert got.dtype == exp.dtype == np.uint8 and got.flags.c_contiguous and exp.flags.c_contiguous
+    return got.size == exp.size and _libc.memcmp(got.ctypes.data, exp.ctypes.data, got.size) == 0
+
+
+def _first_difference(got: np.ndarray, exp: np.ndarray) -> int:
+    return int(np.flatnonzero(got != exp)[0])
+
 
 def _layer_check(w, g, o, retr, store, l, bufs):
     """Compare layer l of the pool and of every staging slot with the oracle's
@@ -178,10 +214,9 @@ def _layer_check(w, g, o, retr, store, l, bufs):
     oracle.store_gather_layer(o.layout, exp_stg, exp_pool, w.block_tables, store)
     got_pool.copy_(g.layers[l])
     got_stg.copy_(g.staging_view().view(S, L, part)[:, l, :].reshape(-1))
-    ok_pool = np.array_equal(got_pool.numpy(), exp_pool)
-    ok_stg = np.array_equal(got_stg.numpy(), exp_stg)
-    assert ok_pool, f"layer {l}: paged tensor differs"
-    assert ok_stg, f"layer {l}: staging differs"
+    gp, gs = got_pool.numpy(), got_stg.numpy()
+    assert _same(gp, exp_pool), f"layer {l}: paged tensor differs at byte {_first_difference(gp, exp_pool)}"
+    assert _same(gs, exp_stg), f"layer {l}: staging differs at byte {_first_difference(gs, exp_stg)}"
     return exp_pool.size + exp_stg.size
 
 
@@ -217,34 +252,7 @@ def _check_layers(w, g, o, retr, store, layers, workers):
     return total
 
 
-def check_full_size_complete(name, workers=8):
-    w = W.make(name)
-    t0 = time.perf_counter()
-    print(f"[complete] {name}: {w.num_reqs} reqs, pool {w.pool_bytes() / 2**30:.1f} GiB, "
-          f"staging {w.staged_bytes() / 2**30:.1f} GiB", flush=True)
-    g = StagingPath(w)
-    g.fill(STG_TAG, POOL_TAG, w.seed)
-    g.prestage()
-    o = OraclePath(w, with_kv=False)
-    o.prestage()
-    sg, so = g.run_pass(validate=True), o.run_pass()
-    torch.cuda.synchronize()
-    assert np.array_equal(g.last_retrieve, so["retrieve"]) and np.array_equal(g.last_store, so["store"])
-    assert sg.num_retrieve > 0 and sg.num_store > 0
-    retr, store = so["retrieve"], so["store"]
-    total = _check_layers(w, g, o, retr, store, range(w.shape.num_layers), workers)
-    print(f"[complete] {name}: {total / 2**30:.1f} GiB compared in {time.perf_counter() - t0:.0f} s", flush=True)
-    del g
-    torch.cuda.synchronize()
-    torch.cuda.empty_cache()
-
-
-@pytest.mark.parametrize("name", ["l32-64x4096", "l80-32x8192"])
-def test_full_size_every_byte(name):
-    check_full_size_complete(name)
-
-
-@pytest.mark.parametrize("name", ["l32-1024x1024-cap50-host", "l32-1024x1024-cap100-host"])
-def test_full_size_sampled_zero_copy_from_host(name):
-    # the capacity sweep's host-staged points in the bench's default zero-copy mode
-    check_full_size(name, lower_tier="zero-copy", complete_edges=True)
+@pytest.mark.parametrize("name", HOST_ZERO_COPY)
+def test_full_size_zero_copy_from_host(name):
+    # host-staged workloads in the bench's default mode: the scatter reads the pinned buffer in place
+    check_full_size(name, lower_tier="zero-copy", layers=_layers(name))
