@@ -86,6 +86,8 @@ def lib() -> ct.CDLL:
     L.or_gather_source.restype = ct.c_int
     L.or_gather_source.argtypes = [ct.POINTER(OrLayout), i32p, ct.c_int32, ct.c_int32, i32p, ct.c_int32,
                                    ct.c_int32, ct.c_int32, i32p]
+    L.or_validate_jobs.restype = ct.c_int
+    L.or_validate_jobs.argtypes = [ct.POINTER(OrLayout), i32p, ct.c_int32, ct.c_int32, i32p, ct.c_int32, ct.c_int]
     L.or_commit_should_stage.restype = ct.c_int
     L.or_commit_should_stage.argtypes = [ct.c_double, ct.c_double, ct.c_uint64, ct.c_uint64, ct.c_uint64,
                                          ct.c_uint64, ct.c_int]
@@ -282,6 +284,20 @@ def gather_source(layout: OrLayout, block_tables: np.ndarray, jobs: np.ndarray,
     f = lib().or_gather_source(ct.byref(layout), _p(bt, ct.c_int32), bt.shape[1], bt.shape[0],
                                _p(jb, ct.c_int32), len(jobs), slot, seg, ct.byref(blk))
     return blk.value if f else None
+
+
+# outcomes of validate_jobs
+VOK, VERANGE, VEDUP = 0, -3, -6
+
+
+def validate_jobs(layout: OrLayout, block_tables: np.ndarray, jobs: np.ndarray, is_store: bool) -> int:
+    """VOK, VERANGE or VEDUP for a job batch against its block tables
+    ([num_reqs, bt_stride]): out-of-range fields or block ids, then two jobs
+    writing one destination (scatter: a paged block; gather: a staging slot)."""
+    bt = np.ascontiguousarray(block_tables, np.int32)
+    jb = np.ascontiguousarray(jobs if len(jobs) else np.zeros((1, 4)), np.int32)
+    return int(lib().or_validate_jobs(ct.byref(layout), _p(bt, ct.c_int32), bt.shape[1], bt.shape[0],
+                                      _p(jb, ct.c_int32), len(jobs), 1 if is_store else 0))
 
 
 def commit_should_stage(ttu: float, ttr: float, free_protected: int, claim_new: int,

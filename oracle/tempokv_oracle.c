@@ -415,6 +415,59 @@ int or_gather_source(const or_layout *lo, const int32_t *bt, int32_t bt_stride, 
 }
 
 /* ------------------------------------------------------------------------- */
+/* Validity of a job batch: the only races a copy launch can have            */
+/* ------------------------------------------------------------------------- */
+
+/* Jobs of one launch run concurrently, so two of them must not write the same
+ * bytes: in the scatter the destinations are paged blocks (a job writes block
+ * bt[req][chunk*C/B + i] of both planes of every layer, so two (job, segment)
+ * pairs naming one block id race), in the gather they are staging slots (two
+ * jobs naming one slot race); any number of jobs may read one slot or block.
+ * A batch is
+ *   OR_VERANGE  if some job has its slot, request or chunk out of range or a
+ *               non-zero reserved field, or names (with those fields in range)
+ *               a block id outside [0, num_blocks);
+ *   OR_VEDUP    otherwise, if two of its destinations coincide;
+ *   OR_VOK      otherwise.
+ * The duplicate test compares every pair of destinations. */
+enum { OR_VOK = 0, OR_VERANGE = -3, OR_VEDUP = -6 };
+
+int or_validate_jobs(const or_layout *lo, const int32_t *bt, int32_t bt_stride, int32_t num_reqs,
+                     const or_job *jobs, int32_t num_jobs, int is_store)
+{
+    int32_t nseg = lo->C / lo->B;
+    for (int32_t q = 0; q < num_jobs; q++) {
+        const or_job *jb = &jobs[q];
+        if (jb->reserved != 0 || !or_job_ok(lo, jb, num_reqs, bt_stride)) return OR_VERANGE;
+        for (int32_t i = 0; i < nseg; i++) {
+            int32_t blk = bt[(int64_t)jb->req * bt_stride + (int64_t)jb->chunk * nseg + i];
+            if (blk < 0 || blk >= lo->num_blocks) return OR_VERANGE;
+        }
+    }
+    for (int32_t q = 0; q < num_jobs; q++) {
+        for (int32_t p = 0; p < q; p++) {
+            if (is_store) {
+                if (jobs[p].slot == jobs[q].slot) return OR_VEDUP;
+                continue;
+            }
+            for (int32_t i = 0; i < nseg; i++)
+                for (int32_t k = 0; k < nseg; k++)
+                    if (bt[(int64_t)jobs[q].req * bt_stride + (int64_t)jobs[q].chunk * nseg + i]
+                        == bt[(int64_t)jobs[p].req * bt_stride + (int64_t)jobs[p].chunk * nseg + k])
+                        return OR_VEDUP;
+        }
+        /* two segments of one job naming the same block */
+        if (!is_store)
+            for (int32_t i = 0; i < nseg; i++)
+                for (int32_t k = 0; k < i; k++)
+                    if (bt[(int64_t)jobs[q].req * bt_stride + (int64_t)jobs[q].chunk * nseg + i]
+                        == bt[(int64_t)jobs[q].req * bt_stride + (int64_t)jobs[q].chunk * nseg + k])
+                        return OR_VEDUP;
+    }
+    return OR_VOK;
+}
+
+/* ------------------------------------------------------------------------- */
 /* Commitment decision (Section 3.2)                                          */
 /* ------------------------------------------------------------------------- */
 

@@ -26,6 +26,7 @@ HASH = ["tests/test_oracle_hash.py", "tests/test_oracle_hash_ref.py", "tests/tes
 LOOKUP = ["tests/test_oracle_lookup.py"]
 COPY = ["tests/test_oracle_copy.py", "tests/test_oracle_properties.py"]
 COMMIT = ["tests/test_oracle_commit.py", "tests/test_oracle_properties.py"]
+VALIDATE = ["tests/test_oracle_validate.py"]
 
 # (name, pin tests, text in the oracle, planted replacement)
 MUTANTS = [
@@ -81,6 +82,16 @@ MUTANTS = [
     ("commit_outcomes_swapped", COMMIT, "return retrieval_requested ? OR_ORDINARY : OR_BLOCKED;",
      "return retrieval_requested ? OR_BLOCKED : OR_ORDINARY;"),
     ("commit_request_not_eligible", COMMIT, "|| (retrieval_requested != 0)", ""),
+    ("validate_reserved_ignored", VALIDATE, "if (jb->reserved != 0 || !or_job_ok(", "if (!or_job_ok("),
+    ("validate_block_bound", VALIDATE, "if (blk < 0 || blk >= lo->num_blocks) return OR_VERANGE;",
+     "if (blk < 0 || blk > lo->num_blocks) return OR_VERANGE;"),
+    ("validate_job_compared_with_itself", VALIDATE, "for (int32_t p = 0; p < q; p++) {", "for (int32_t p = 0; p <= q; p++) {"),
+    ("validate_within_job_unchecked", VALIDATE, "for (int32_t k = 0; k < i; k++)", "for (int32_t k = 0; k < 0; k++)"),
+    ("validate_store_slots_unchecked", VALIDATE, "if (jobs[p].slot == jobs[q].slot) return OR_VEDUP;",
+     "if (jobs[p].slot == jobs[q].slot && 0) return OR_VEDUP;"),
+    ("validate_same_segment_only", VALIDATE,
+     "== bt[(int64_t)jobs[p].req * bt_stride + (int64_t)jobs[p].chunk * nseg + k])",
+     "== bt[(int64_t)jobs[p].req * bt_stride + (int64_t)jobs[p].chunk * nseg + i])"),
 ]
 
 def _compile(src_text: str, out: str) -> None:
@@ -100,7 +111,7 @@ def test_unplanted_copy_passes_the_pins(tmp_path):
     # the harness itself: the oracle as committed, built the same way, passes every pin
     so = str(tmp_path / "liboracle_ref.so")
     _compile(open(SRC).read(), so)
-    r = _run_pins(so, sorted(set(HASH + LOOKUP + COPY + COMMIT)))
+    r = _run_pins(so, sorted(set(HASH + LOOKUP + COPY + COMMIT + VALIDATE)))
     assert r.returncode == 0, r.stdout[-3000:]
 
 
