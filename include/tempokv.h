@@ -20,6 +20,9 @@
  *                         retrieve gated on those copies (stage-ready)
  *   kv_sim_run            claim/commitment controller in a discrete-event
  *                         simulation (Sections 3.1-3.3)
+ *   kv_validate_jobs(_device)  race check of a job batch (duplicate
+ *                         destinations, out-of-range ids), on host copies or
+ *                         on the device
  *
  * Conventions shared by every call
  * --------------------------------
@@ -347,6 +350,23 @@ int kv_retrieve_pipelined(kv_pipeline *pl, const kv_layout *layout, const void *
  * else KV_OK. */
 int kv_validate_jobs(const kv_layout *layout, const int32_t *h_block_tables, int32_t bt_stride,
                      int32_t num_reqs, const kv_job *h_jobs, int32_t num_jobs, int is_store);
+
+/* The same check on the device, for a batch whose jobs and block tables are
+ * already in device memory (race detection before a scatter or gather: two
+ * jobs of one launch writing the same paged block or staging slot are the
+ * only writes that can race; many jobs may read one slot).  d_marks is
+ * caller-owned device scratch of 2 + (is_store ? num_slots : num_blocks)
+ * int32, overwritten; d_status (one int32 in device memory) receives
+ * KV_ERANGE, KV_EDUP or KV_OK, with the meaning and precedence of
+ * kv_validate_jobs, once the enqueued work completes: read it after `stream`
+ * synchronizes.  Three launches on `stream` (clear, mark, status), no
+ * allocation, no memset, no host synchronization.  Returns KV_OK once
+ * enqueued; KV_EINVAL (bad layout, negative count, null pointer) or KV_EALIGN
+ * (d_jobs not 16-byte aligned, an int32 pointer not 4-byte aligned) with
+ * nothing enqueued; KV_EHIP if a launch fails. */
+int kv_validate_jobs_device(const kv_layout *layout, const int32_t *d_block_tables, int32_t bt_stride,
+                            int32_t num_reqs, const kv_job *d_jobs, int32_t num_jobs, int is_store,
+                            int32_t *d_marks, int32_t *d_status, void *stream);
 
 /* ----------------------------------------------------------------------- */
 /* Commitment rule (host)                                                   */

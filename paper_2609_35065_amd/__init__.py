@@ -38,7 +38,7 @@ EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_in
            "kv_validate_jobs", "kv_commit_should_stage", "kv_commit_should_stage_n", "kv_strerror",
            "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out",
            "kv_pipeline_create", "kv_pipeline_destroy", "kv_retrieve_pipelined", "kv_decide_claims",
-           "kv_build_jobs_routed", "kv_ttr_static", "kv_ttr_state_aware", "kv_chunk_keys"]
+           "kv_build_jobs_routed", "kv_ttr_static", "kv_ttr_state_aware", "kv_chunk_keys", "kv_validate_jobs_device"]
 # the calls that run on the host only (host.cpp, controller.cpp)
 HOST_CALLS = ["kv_build_jobs", "kv_build_jobs_routed", "kv_decide_claims", "kv_group_jobs_by_slot",
               "kv_validate_jobs", "kv_commit_should_stage", "kv_commit_should_stage_n", "kv_retrieve_plan",
@@ -103,6 +103,7 @@ SIGNATURES = {
     "kv_retrieve_scatter_as": [_i32, ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
     "kv_group_jobs_by_slot": [_vp, _i32],
     "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
+    "kv_validate_jobs_device": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int, _vp, _vp, _vp],
     "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
     "kv_commit_should_stage_n": [_i32, _vp, _vp, _u64, _vp, _vp, _u64, _vp, _vp],
     "kv_ttr_static": [_i32, _vp, _i32, _vp, _vp, _dbl, ct.POINTER(_dbl)],
@@ -581,6 +582,22 @@ def kv_validate_jobs(layout: KvLayout, block_tables: np.ndarray, jobs: np.ndarra
     if rc not in (KV_OK, KV_ERANGE, KV_EDUP):
         raise KvError(rc, "kv_validate_jobs")
     return rc
+
+
+def kv_validate_jobs_device(layout: KvLayout, d_block_tables, bt_stride: int, num_reqs: int, d_jobs, num_jobs: int,
+                            is_store: bool, d_marks, d_status, stream=None) -> None:
+    """Enqueue the device form of kv_validate_jobs: d_status (int32 device
+    tensor of one element) receives KV_OK, KV_ERANGE or KV_EDUP; d_marks is
+    int32 device scratch of 2 + (num_slots if is_store else num_blocks)."""
+    import torch
+    need = 2 + (layout.num_slots if is_store else layout.num_blocks)
+    if not isinstance(d_marks, int) and d_marks.numel() < need:
+        raise ValueError(f"d_marks holds {d_marks.numel()} int32, needs {need}")
+    _check(lib().kv_validate_jobs_device(ct.byref(layout), _dptr(d_block_tables, torch.int32, "block_tables"),
+                                         bt_stride, num_reqs, _dptr(d_jobs, torch.int32, "jobs"), num_jobs,
+                                         1 if is_store else 0, _dptr(d_marks, torch.int32, "marks"),
+                                         _dptr(d_status, torch.int32, "status"), _stream(stream)),
+           "kv_validate_jobs_device")
 
 
 def kv_commit_should_stage(ttu_s: float, ttr_s: float, free_protected_bytes: int, claim_new_bytes: int,

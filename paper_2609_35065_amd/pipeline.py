@@ -54,10 +54,11 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (KV_COMMIT, KV_ORDINARY, KV_RETRIEVE_QUAD, KV_RETRIEVE_STREAM, RETRIEVE_KIND_NAMES, KvIndex,
+from . import (KV_COMMIT, KV_OK, KV_ORDINARY, KV_RETRIEVE_QUAD, KV_RETRIEVE_STREAM, RETRIEVE_KIND_NAMES, KvIndex,
                KvLayout, KvPipeline, kv_build_jobs_routed, kv_chunk_keys, kv_decide_claims,
                kv_group_jobs_by_slot, kv_hash_prefix, kv_host_device_pointer, kv_lookup, kv_retrieve_pipelined,
-               kv_retrieve_plan, kv_retrieve_scatter_as, kv_stage_in, kv_stage_out, kv_store_gather, make_layout)
+               kv_retrieve_plan, kv_retrieve_scatter_as, kv_stage_in, kv_stage_out, kv_store_gather,
+               kv_validate_jobs_device, make_layout)
 
 LOWER_TIER_MODES = ("zero-copy", "pipelined", "serialized")
 
@@ -149,6 +150,7 @@ class StagingPath:
         self.last_store = np.zeros((0, 4), np.int32)
         self.last_decisions = np.zeros(0, np.int32)
         self.retrieve_kind: Optional[int] = None
+        self._val_marks: Optional[torch.Tensor] = None   # scratch of the device race check (validate=True)
         # planned retrieve variant -> variant to run instead (set by tune_retrieve)
         self.retrieve_choice: Dict[int, int] = {}
         self._last_nres = 0
@@ -263,7 +265,10 @@ class StagingPath:
         torch.cuda.Event is appended under "hash", "lookup", "retrieve",
         "ordinary" and "store" around each launch, recorded on the stream it
         runs on.  ``claims``: the commitment inputs (default: every request
-        runs now and the budget is the whole staging buffer)."""
+        runs now and the budget is the whole staging buffer).  ``validate``
+        (debug): the job lists are checked on the host and, once uploaded, on
+        the device (kv_validate_jobs, kv_validate_jobs_device) before any copy
+        is launched."""
         self.launch_lookup(timers)
         return self.complete_pass(evict_stored, validate, timers, claims)
 
@@ -349,6 +354,8 @@ class StagingPath:
                 self.h_store.numpy()[:ns] = store
                 self.d_store[:ns].copy_(self.h_store[:ns], non_blocking=True)
             self._uploaded[par].record(self.stream)
+            if validate:
+                self._validate_on_device(nr + no, ns)
             e = self._ev(timers, "retrieve")
             # the copy variant suited to how these jobs share staged chunks
             planned = kv_retrieve_plan(self.layout, self.h_retr.numpy()[:nres])
@@ -407,6 +414,24 @@ class StagingPath:
         if evict_stored and ns:
             self.evict_last()
         return st
+
+    def _validate_on_device(self, n_retr: int, n_store: int) -> None:
+        """Debug check of the uploaded job lists on this path's stream
+        (kv_validate_jobs_device): raises before any copy of the pass is
+        launched if a list names an out-of-range id or two jobs of one launch
+        write the same block or slot."""
+        w = self.batch
+        if self._val_marks is None:
+            self._val_marks = torch.empty(2 + max(self.w.num_blocks, self.w.num_slots), dtype=torch.int32,
+                                          device=self.dev)
+            self._val_status = torch.empty(2, dtype=torch.int32, device=self.dev)
+        kv_validate_jobs_device(self.layout, self.bt, w.bt_stride, w.num_reqs, self.d_retr, n_retr, False,
+                                self._val_marks, self._val_status[0:1], self.stream)
+        kv_validate_jobs_device(self.layout, self.bt, w.bt_stride, w.num_reqs, self.d_store, n_store, True,
+                                self._val_marks, self._val_status[1:2], self.stream)
+        self.stream.synchronize()
+        got = [int(x) for x in self._val_status.cpu()]
+        assert got == [KV_OK, KV_OK], f"device job check: retrieve {got[0]}, store {got[1]}"
 
     def tune_retrieve(self, reps: int = 5) -> Dict[str, float]:
         """Choose, for this path's paged pool, between the planned retrieve and

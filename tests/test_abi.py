@@ -161,6 +161,22 @@ def test_copy_calls_reject_bad_layouts_before_any_launch(over, code):
         assert f(ct.byref(lo), 0x10000, layers, 0x10000, 10, 2, 0x10000, 1, None) == code
 
 
+def test_device_validate_rejects_bad_arguments_before_any_launch():
+    L = kv.lib()
+    f = L.kv_validate_jobs_device
+    A, J, M, S = 0x10000, 0x20000, 0x30000, 0x40000      # block tables, jobs, marks, status (never dereferenced)
+    for over in (dict(num_layers=0), dict(chunk_tokens=24), dict(num_blocks=0), dict(num_slots=0)):
+        assert f(ct.byref(_layout(**over)), A, 10, 2, J, 1, 0, M, S, None) == kv.KV_EINVAL
+    lo = _layout()
+    for args in ((A, 10, 2, J, -1, 0, M, S), (A, 10, -1, J, 1, 0, M, S), (A, 0, 2, J, 1, 0, M, S),
+                 (A, 10, 2, J, 1, 0, None, S), (A, 10, 2, J, 1, 0, M, None), (None, 10, 2, J, 1, 1, M, S),
+                 (A, 10, 2, None, 1, 1, M, S)):
+        assert f(ct.byref(lo), *args, None) == kv.KV_EINVAL, args
+    for args in ((A, 10, 2, J + 8, 1, 0, M, S), (A, 10, 2, J, 1, 0, M + 2, S), (A, 10, 2, J, 1, 0, M, S + 1),
+                 (A + 2, 10, 2, J, 1, 0, M, S)):
+        assert f(ct.byref(lo), *args, None) == kv.KV_EALIGN, args
+
+
 def test_copy_calls_reject_bad_pointers_before_any_launch():
     lo = _layout()
     L = kv.lib()
