@@ -274,3 +274,55 @@ def test_ttr_argument_errors():
         kv.kv_ttr_static([0], [1.0], [0], 0.0)                  # rate <= 0
     with pytest.raises(kv.KvError):
         kv.kv_ttr_state_aware([0], [1.0], [0], [0], [0.0], math.nan, 0.0, 1.0)
+
+
+# ---------------------------------------------------------------------------
+# properties of the rule that hold for any batch (Section 3.2), on both sides
+# ---------------------------------------------------------------------------
+
+def _decide(impl, o, w, hit, cs, cl):
+    if impl == "oracle":
+        return list(o.decide_claims(hit, cs, cl))
+    return kv.kv_decide_claims(hit, cs, o.chunk_off, cl.ttu, cl.ttr, cl.requested, SB, cl.budget_bytes,
+                               w.num_slots)[0].tolist()
+
+
+@pytest.mark.parametrize("impl", ["oracle", "library"])
+@pytest.mark.parametrize("seed", range(25))
+def test_rule_properties(impl, seed):
+    rng = np.random.default_rng(500 + seed)
+    o, w = _oracle_path(int(rng.integers(1, 14)), seed=seed + 300)
+    hit, cs, cl = _random_case(rng, o)
+    R = len(hit)
+    eligible = (cl.ttu <= cl.ttr) | cl.requested
+    d = _decide(impl, o, w, hit, cs, cl)
+    for r in range(R):
+        # a requested claim commits or takes the ordinary path; a waiting one commits, defers or stays planned
+        allowed = {oracle.COMMIT, oracle.ORDINARY} if cl.requested[r] else {oracle.COMMIT, oracle.DEFER, oracle.BLOCKED}
+        assert d[r] in allowed
+        assert (d[r] == oracle.DEFER) == (not eligible[r])
+    # enough budget for every object of the batch: every eligible claim commits
+    everything = Claims(cl.requested, cl.ttu, cl.ttr, w.num_slots * SB)
+    d = _decide(impl, o, w, hit, cs, everything)
+    assert d == [oracle.COMMIT if e else oracle.DEFER for e in eligible]
+    # no budget: only claims without objects can commit
+    nothing = Claims(cl.requested, cl.ttu, cl.ttr, 0)
+    d = _decide(impl, o, w, hit, cs, nothing)
+    for r in range(R):
+        if not eligible[r]:
+            assert d[r] == oracle.DEFER
+        elif hit[r] == 0:
+            assert d[r] == oracle.COMMIT
+        else:
+            assert d[r] == (oracle.ORDINARY if cl.requested[r] else oracle.BLOCKED)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_library_ledger_stays_within_budget(seed):
+    rng = np.random.default_rng(700 + seed)
+    o, w = _oracle_path(int(rng.integers(1, 14)), seed=seed + 400)
+    hit, cs, cl = _random_case(rng, o)
+    d, prot, reserved = kv.kv_decide_claims(hit, cs, o.chunk_off, cl.ttu, cl.ttr, cl.requested, SB,
+                                            cl.budget_bytes, w.num_slots)
+    assert reserved <= cl.budget_bytes
+    assert reserved == int(np.count_nonzero(prot)) * SB
