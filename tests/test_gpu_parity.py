@@ -338,6 +338,45 @@ def test_index_updates_small_and_large_batches():
     idx.destroy()
 
 
+def test_index_large_table_update_limits():
+    # A table of 2^21 positions (a million staged chunks): incremental uploads are capped at 65,536 changed
+    # entries rather than an eighth of the table.  Inserts and erases at, just over and well under that cap
+    # (incremental, whole image, incremental), each followed by a device lookup of every key.
+    rng = np.random.default_rng(33)
+    keys = np.unique(rng.integers(1, 2**63, 200000, dtype=np.int64)).astype(np.uint64)
+    rng.shuffle(keys)
+    idx = kv.KvIndex(1 << 20)
+    ref = {}
+
+    def check(tag):
+        # one-block chunks in requests of 64 keys: every key's slot in chunk_slot, absent keys -1
+        n = keys.size
+        blk_off = np.arange(0, n + 64, 64, dtype=np.int64)
+        blk_off[-1] = n
+        cs, _ = _lookup_gpu(idx, keys, blk_off, 1)
+        want = np.array([ref.get(int(k), -1) for k in keys], np.int32)
+        assert np.array_equal(cs, want), tag
+        assert idx.size() == len(ref), tag
+
+    pos = 0
+    for n in (16, 65536, 65537, 1000):     # the first upload of an index sends its whole table
+        batch = keys[pos:pos + n]
+        pos += n
+        slots = rng.integers(0, 1 << 20, n).astype(np.int32)
+        idx.insert(batch, slots)
+        ref.update(zip((int(k) for k in batch), (int(s) for s in slots)))
+        check(("insert", n))
+    live = np.array(list(ref.keys()), np.uint64)
+    for n in (65536, 65537, 10):
+        gone = live[:n]
+        live = live[n:]
+        idx.erase(gone)
+        for k in gone:
+            ref.pop(int(k))
+        check(("erase", n))
+    idx.destroy()
+
+
 def test_out_of_range_jobs_are_skipped_on_device():
     shape = W.KVShape(2, 2, 64, 2, 16, 64)
     w = W.small_random(21, shape, num_reqs=4, max_len=256)
