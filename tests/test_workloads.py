@@ -119,3 +119,13 @@ def test_random_shapes_respect_the_layout_rules():
         assert sh.seg_bytes % 16 == 0
     assert W.random_shapes(2026, 40) == shapes                      # seeded
     assert {sh.elem_bytes for sh in shapes} == {1, 2, 4}
+
+
+def test_pool_holds_the_live_blocks_of_many_short_requests():
+    # eight one-token requests with 32-token blocks: 8 live blocks, though 1.5 x 8 tokens fit in one block
+    shape = W.KVShape(1, 1, 16, 2, 32, 32)
+    w = W._assemble("short", shape, 1, [1] * 8, [-1] * 8, [0] * 8, 0, prestage=[], num_slots=4, pool_factor=1.5)
+    assert w.num_blocks == 8
+    assert sorted(w.block_tables[:, 0].tolist()) == list(range(8))
+    # the configurations' pools are sized by their tokens as before
+    assert W.make("l32-64x4096").num_blocks == 20480 and W.make("l80-32x8192").num_blocks == 18023

@@ -334,7 +334,9 @@ def _assemble(name, shape, seed, lengths, prefix_id, prefix_tokens, n_prefixes,
     B = shape.block_size
     need = (lengths + B - 1) // B
     if pool_blocks is None:
-        pool_blocks = int(math.ceil(pool_factor * lengths.sum() / B))
+        # the factor applies to the tokens; every request also rounds its tail up to a whole block, so many
+        # short requests can need more blocks than that: never fewer than the live blocks
+        pool_blocks = max(int(math.ceil(pool_factor * lengths.sum() / B)), int(need.sum()))
     assert pool_blocks >= need.sum(), "pool smaller than the live blocks"
     perm = _rng(seed, _P_PERM).permutation(pool_blocks).astype(np.int32)
     bt_stride = int(need.max()) if R else 1
