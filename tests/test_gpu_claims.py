@@ -82,3 +82,59 @@ def test_default_claims_all_commit_and_match_previous_jobs():
         assert np.array_equal(g.last_retrieve, so["retrieve"]) and np.array_equal(g.last_store, so["store"])
         for l in range(len(g.layers)):
             assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l])
+
+
+def test_random_shapes_modes_and_claims():
+    # TEMPOKV_CLAIM_SHAPES random shapes (40 by default) drawn from TEMPOKV_CLAIM_SEED (777 by default), each
+    # in one of the four modes with a random batch, pipeline batch size, overlapped or serial passes, paged
+    # layout and padding; three passes with random commitment inputs and eviction, each compared in full.
+    import os
+    n = int(os.environ.get("TEMPOKV_CLAIM_SHAPES", "40"))
+    seed = int(os.environ.get("TEMPOKV_CLAIM_SEED", "777"))
+    modes = ["hbm", "zero-copy", "pipelined", "serialized"]
+    seen = set()
+    for k, shape in enumerate(W.random_shapes(seed, n)):
+        rng = np.random.default_rng(seed * 11 + k)
+        mode = modes[k % 4]
+        w = W.small_random(seed * 13 + k, shape, num_reqs=int(rng.integers(2, 16)),
+                           max_len=int(rng.integers(1, 5)) * shape.chunk_tokens + int(rng.integers(0, 40)),
+                           n_prefixes=int(rng.integers(1, 4)), paged_layout=["kv_first", "block_first"][k % 2],
+                           block_pad=[0, 16, 4096][k % 3])
+        if mode != "hbm":
+            w.staging_in_host = True
+        g = StagingPath(w, lower_tier="zero-copy" if mode == "hbm" else mode,
+                        slots_per_batch=int(rng.integers(1, 5)), overlap=bool(k % 3 == 0))
+        g.fill(STG_TAG, POOL_TAG, w.seed)
+        g.prestage()
+        o = OraclePath(w, kv_seed=w.seed, staging_tag=STG_TAG, pool_tag_base=POOL_TAG)
+        o.prestage()
+        for p in range(3):
+            R = w.num_reqs
+            cl = ClaimInputs(rng.random(R) < 0.6, rng.choice([-1.0, 0.0, 0.5, 3.0], R),
+                             rng.choice([0.0, 1.0, 2.0], R), int(rng.integers(0, 6)) * w.shape.slot_bytes)
+            evict = bool(rng.random() < 0.5)
+            g.run_pass(validate=True, claims=cl, evict_stored=evict)
+            so = o.run_pass(claims=cl, evict_stored=evict)
+            torch.cuda.synchronize()
+            tag = (k, mode, p, shape)
+            assert np.array_equal(g.last_decisions, so["decisions"]), tag
+            assert np.array_equal(g.last_retrieve, so["retrieve"]), tag
+            assert np.array_equal(g.last_ordinary, so["ordinary"]), tag
+            assert np.array_equal(g.last_store, so["store"]), tag
+            assert np.array_equal(g.staging_view().cpu().numpy(), o.staging), tag
+            for l in range(len(g.layers)):
+                assert np.array_equal(g.layers[l].cpu().numpy(), o.layers[l]), tag + (l,)
+            if g.staged_mode:
+                hb = g.staging.cpu().numpy().reshape(w.num_slots, -1)
+                hh = g.staging_host.numpy().reshape(w.num_slots, -1)
+                assert np.array_equal(hb[g.resident], hh[g.resident]), tag
+            seen |= set(int(d) for d in so["decisions"])
+            if rng.random() < 0.5:
+                g.drop_fast_tier()
+        del g, o
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        if k % 100 == 99:
+            print(f"[claims] {k + 1}/{n} shapes ok", flush=True)
+    if n >= 40:
+        assert {kv.KV_COMMIT, kv.KV_ORDINARY, kv.KV_BLOCKED, kv.KV_DEFER} <= seen, seen

@@ -557,20 +557,22 @@ def test_million_job_lists_match_oracle(kind):
 
 
 def test_many_random_shapes_every_variant():
-    # A wider sweep than the forty above: TEMPOKV_SOAK_SHAPES random shapes (300 by default; 3,000 have been
-    # run), each with two whole passes and then every retrieve variant on a random job list (grouped or not),
-    # every byte compared with the oracle.
+    # A wider sweep than the forty above: TEMPOKV_SOAK_SHAPES random shapes (300 by default) drawn from
+    # TEMPOKV_SOAK_SEED (3030 by default), each with two whole passes and then every retrieve variant on a
+    # random job list (grouped or not), every byte compared with the oracle.
     n = int(os.environ.get("TEMPOKV_SOAK_SHAPES", "300"))
-    for k, shape in enumerate(W.random_shapes(3030, n)):
+    seed = os.environ.get("TEMPOKV_SOAK_SEED")
+    shape_seed, wl_seed = (3030, 5000) if seed is None else (int(seed), 7 * int(seed))
+    for k, shape in enumerate(W.random_shapes(shape_seed, n)):
         layout = ["kv_first", "block_first"][k % 2]
         pad = [0, 16, 4096, 48, 32][k % 5]
-        w = W.small_random(5000 + k, shape, num_reqs=5 + k % 4, max_len=3 * shape.chunk_tokens + 7 * (k % 5),
+        w = W.small_random(wl_seed + k, shape, num_reqs=5 + k % 4, max_len=3 * shape.chunk_tokens + 7 * (k % 5),
                            paged_layout=layout, block_pad=pad)
         g, o = _pair(w)
         for p in range(2):
             sg, so = g.run_pass(validate=True), o.run_pass()
             _compare_pass(g, o, sg, so)
-        jobs = W.random_retrieve_jobs(w, 5000 + k, slots_used=max(1, w.num_slots // 3))
+        jobs = W.random_retrieve_jobs(w, wl_seed + k, slots_used=max(1, w.num_slots // 3))
         if len(jobs):
             jobs = np.ascontiguousarray(kv.kv_group_jobs_by_slot(jobs) if k % 2 else jobs, np.int32)
             d_jobs = torch.from_numpy(jobs).cuda()
