@@ -118,7 +118,9 @@ def _label(symbol: str) -> str:
                       ("copy_generic_kernel<false>", "store gather, generic path"),
                       ("hash_kernel", "prefix hash (kv_hash_prefix)"),
                       ("lookup_kernel", "lookup (kv_lookup)"),
-                      ("index_apply_kernel", "index update (kv_index_insert / erase)")):
+                      ("index_apply_kernel", "index update (kv_index_insert / erase)"),
+                      ("mixed_traffic_kernel", "measurement reference: the retrieve's bytes, no dependence "
+                                               "(kv_probe_mixed_traffic)")):
         if key in symbol:
             return text
     if "group_copy_kernel" in symbol:
@@ -310,14 +312,16 @@ def summarize_ceiling(directory: str, workload: str, calibration: str = None):
         for r in rows:
             if "reduce_kernel" in r["Kernel_Name"]:
                 per_reader[_short_symbol(r["Kernel_Name"]).split("<")[0]] += float(r["Counter_Value"])
+        mixed = [float(r["Counter_Value"]) for r in rows if _short_symbol(r["Kernel_Name"]) == "mixed_traffic_kernel"]
         res[kind] = (statistics.median(v for _, v in mine[-n:]) * scale * 1024,
-                     sum(per_reader.values()) / n * scale * 1024, len(mine))
+                     sum(per_reader.values()) / n * scale * 1024, len(mine),
+                     statistics.median(mixed) * scale * 1024 if mixed else None)
     c = d["ceiling"]
     cmds = dict(profile_commands(workload, "gpurun_out/prof_" + workload))
     cal_wl = os.path.basename(os.path.normpath(cal_dir))[len("prof_"):] or workload
     cmds.update({k: v for k, v in profile_commands(cal_wl, "gpurun_out/prof_" + cal_wl) if k.startswith("cal_")})
-    wo_read, rd_read, nl = res["ceil_fetch"]
-    wo_write, rd_write, _ = res["ceil_write"]
+    wo_read, rd_read, nl, ix_read = res["ceil_fetch"]
+    wo_write, rd_write, _, ix_write = res["ceil_write"]
     txt = [f"# HBM traffic of the retrieve's same-pool ceiling, workload {workload}",
            "# Made by `python bench.py --summarize-ceiling` from these runs (repository root, one MI355X):",
            *[f"#   {cmds[k]}" for k in ("ceil_fetch", "ceil_write", "cal_fetch", "cal_write")],
@@ -335,6 +339,11 @@ def summarize_ceiling(directory: str, workload: str, calibration: str = None):
            f"unique_read_hbm_read_bytes_per_pass={rd_read:.0f}",
            f"unique_read_hbm_write_bytes_per_pass={rd_write:.0f}",
            f"ceiling_traffic_bytes={wo_read + wo_write + rd_read + rd_write:.0f}"]
+    if ix_read is not None and ix_write is not None:
+        txt += ["# kv_probe_mixed_traffic (mixed_traffic_kernel, the same algorithmic bytes in one launch with no",
+                "# dependence between its reads and writes): median over its launches in the run",
+                f"independent_mix_hbm_read_bytes_per_launch={ix_read:.0f}",
+                f"independent_mix_hbm_write_bytes_per_launch={ix_write:.0f}"]
     if isinstance(c, dict) and "writes_with_unique_read" in c:
         txt.append(f"# timings of this run are not quoted: counter collection serialises the two streams")
     path = os.path.join(PROFILES, f"traffic_retrieve_ceiling_{workload}.txt")
@@ -439,7 +448,11 @@ def _retrieve_write_bound(path, torch, reps: int = CEILING_REPS):
     destination blocks, but every job reading one staged chunk (which stays in
     L2), so HBM sees only the scattered 32 KiB writes.  Its time bounds the
     retrieve on this pool from below; it runs after the timed steps and
-    leaves the written blocks holding that chunk."""
+    leaves the written blocks holding that chunk.  Before it, the same
+    algorithmic bytes are moved by kv_probe_mixed_traffic (reads and writes
+    interleaved in one launch with no dependence between them), and after
+    it the writes run together with a read of the unique chunks on a second
+    stream."""
     import numpy as np
     import paper_2609_35065_amd as kv
     n = path._last_nres
@@ -448,11 +461,28 @@ def _retrieve_write_bound(path, torch, reps: int = CEILING_REPS):
             kv.KV_RETRIEVE_UNIT, kv.KV_RETRIEVE_PAIR, kv.KV_RETRIEVE_QUAD):
         return None
     w = path.batch
+    s = path.stream
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    slots = np.unique(path.h_retr.numpy()[:n, 0])
+    sb = w.shape.slot_bytes
+    uniq = int(slots.size) * sb
+    written = n * sb
+    # First, the same algorithmic bytes with no dependence between reads and writes, in one launch
+    # (kv_probe_mixed_traffic: the unique staged chunks read, the destination blocks written with a
+    # filler, interleaved).  It overwrites the destinations; the writes-only launches below rewrite them.
+    d_slots = torch.from_numpy(slots.astype(np.int32)).to(path.dev)
+    mix = []
+    for _ in range(reps):
+        a.record(s)
+        kv.kv_probe_mixed_traffic(path.layout, path.staging_ptr, path.layers, path.bt, w.bt_stride, w.num_reqs,
+                                  path.d_retr, n, d_slots, int(slots.size), 0x5A5A5A5A, s)
+        b.record(s)
+        b.synchronize()
+        mix.append(a.elapsed_time(b))
+    t_ix = float(np.median(mix))
     jobs = path.h_retr.numpy()[:n].copy()
     jobs[:, 0] = jobs[0, 0]
     d_jobs = torch.from_numpy(jobs).to(path.dev)
-    s = path.stream
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ms = []
     for _ in range(reps):
         a.record(s)
@@ -462,23 +492,23 @@ def _retrieve_write_bound(path, torch, reps: int = CEILING_REPS):
         b.synchronize()
         ms.append(a.elapsed_time(b))
     t = float(np.median(ms))
-    written = n * w.shape.slot_bytes
     out = {"ms": round(t, 4), "GB/s_written": round(written / (t * 1e-3) / 1e9, 1),
            "what": "the timed retrieve's jobs and variant with every job reading one staged chunk: its "
                    f"scattered writes alone (median of {reps})"}
+    out["independent_mix"] = {
+        "ms": round(t_ix, 4), "GB/s_alg": round((uniq + written) / (t_ix * 1e-3) / 1e9, 1),
+        "what": "kv_probe_mixed_traffic: the unique staged chunks read and the destination blocks written, "
+                f"interleaved in one launch with no data passing between them (median of {reps})"}
     # The same writes with the unique staged chunks read from HBM at the same time, on a second stream:
     # the retrieve's algorithmic bytes (unique reads + writes) with no kernel of ours reading them.  The
     # reads are torch reductions over the contiguous runs of the chunks' slots.
-    slots = np.unique(path.h_retr.numpy()[:n, 0])
     runs, start = [], int(slots[0])
     for prev, cur in zip(slots[:-1], slots[1:]):
         if cur != prev + 1:
             runs.append((start, int(prev) + 1))
             start = int(cur)
     runs.append((start, int(slots[-1]) + 1))
-    sb = w.shape.slot_bytes
     views = [path.staging[r0 * sb:r1 * sb].view(torch.int64) for r0, r1 in runs]
-    uniq = int(slots.size) * sb
     s2 = torch.cuda.Stream()
     sink = torch.zeros(len(views), dtype=torch.int64, device=path.dev)
 
@@ -982,6 +1012,8 @@ def main() -> int:
             wb["retrieve_frac_of_this_rate"] = round(wb["alg_bytes_at_this_rate_ms"] / k_ms["retrieve"], 4)
             mx = wb["writes_with_unique_read"]
             mx["retrieve_frac_of_this_ceiling"] = round(mx["ms"] / k_ms["retrieve"], 4)
+            ix = wb["independent_mix"]
+            ix["retrieve_speedup_over_this"] = round(ix["ms"] / k_ms["retrieve"], 4)
             line["practical_peak"]["retrieve_writes_only"] = wb
         if w.staging_in_host:
             line["practical_peak"].update(_host_link_gbs(torch))

@@ -535,6 +535,27 @@ int kv_sim_run(const kv_sim_config *cfg, const double *h_obj_bytes, int32_t num_
                int64_t trace_cap, int64_t *trace_len);
 
 /* ----------------------------------------------------------------------- */
+/* Measurement reference (not part of the path)                             */
+/* ----------------------------------------------------------------------- */
+
+/* For callers that time the retrieve against what its bytes cost on their
+ * own pool: moves kv_retrieve_scatter's algorithmic bytes with no dependence
+ * between them, in one launch.  Every segment of the num_read_slots slots in
+ * d_slots (int32, device) is read once, and every destination segment of the
+ * jobs (the blocks kv_retrieve_scatter would write) is written with the
+ * 32-bit word `fill` repeated; the reads are spread evenly among the writes
+ * in dispatch order, and no written byte depends on a read.  It OVERWRITES
+ * those destination blocks (re-run the retrieve to restore them) and touches
+ * nothing else; jobs, slots and block ids out of range are skipped as in the
+ * copies.  Same layout and pointer arguments as kv_retrieve_scatter; one
+ * launch per call.  Errors: KV_EINVAL (also when the jobs' and slots'
+ * segments number 2^31 or more), KV_EALIGN, KV_EHIP. */
+int kv_probe_mixed_traffic(const kv_layout *layout, const void *d_staging, void *const *h_layer_ptrs,
+                           const int32_t *d_block_tables, int32_t bt_stride, int32_t num_reqs,
+                           const kv_job *d_jobs, int32_t num_jobs, const int32_t *d_slots,
+                           int32_t num_read_slots, uint32_t fill, void *stream);
+
+/* ----------------------------------------------------------------------- */
 /* Misc                                                                     */
 /* ----------------------------------------------------------------------- */
 

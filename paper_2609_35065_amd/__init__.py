@@ -38,7 +38,8 @@ EXPORTS = ["kv_hash_prefix", "kv_index_create", "kv_index_destroy", "kv_index_in
            "kv_validate_jobs", "kv_commit_should_stage", "kv_commit_should_stage_n", "kv_strerror",
            "kv_host_device_pointer", "kv_version", "kv_sim_run", "kv_stage_in", "kv_stage_out",
            "kv_pipeline_create", "kv_pipeline_destroy", "kv_retrieve_pipelined", "kv_decide_claims",
-           "kv_build_jobs_routed", "kv_ttr_static", "kv_ttr_state_aware", "kv_chunk_keys", "kv_validate_jobs_device"]
+           "kv_build_jobs_routed", "kv_ttr_static", "kv_ttr_state_aware", "kv_chunk_keys", "kv_validate_jobs_device",
+           "kv_probe_mixed_traffic"]
 # the calls that run on the host only (host.cpp, controller.cpp)
 HOST_CALLS = ["kv_build_jobs", "kv_build_jobs_routed", "kv_decide_claims", "kv_group_jobs_by_slot",
               "kv_validate_jobs", "kv_commit_should_stage", "kv_commit_should_stage_n", "kv_retrieve_plan",
@@ -79,7 +80,7 @@ _lib: Optional[ct.CDLL] = None
 # Tests only: a separately built copy of the host-only calls (HOST_CALLS) from the same sources, e.g. a
 # sanitizer build, used by the host-call wrappers in place of libtempokv.so.
 _host_override: Optional[ct.CDLL] = None
-_vp, _i32, _i64, _u64, _dbl = ct.c_void_p, ct.c_int32, ct.c_int64, ct.c_uint64, ct.c_double
+_vp, _i32, _i64, _u32, _u64, _dbl = ct.c_void_p, ct.c_int32, ct.c_int64, ct.c_uint32, ct.c_uint64, ct.c_double
 
 SIGNATURES = {
     "kv_hash_prefix": [_vp, _vp, _i32, _u64, _vp, _vp, _vp],
@@ -102,6 +103,7 @@ SIGNATURES = {
     "kv_retrieve_plan": [ct.POINTER(KvLayout), _vp, _i32],
     "kv_retrieve_scatter_as": [_i32, ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp],
     "kv_group_jobs_by_slot": [_vp, _i32],
+    "kv_probe_mixed_traffic": [ct.POINTER(KvLayout), _vp, _vp, _vp, _i32, _i32, _vp, _i32, _vp, _i32, _u32, _vp],
     "kv_validate_jobs": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int],
     "kv_validate_jobs_device": [ct.POINTER(KvLayout), _vp, _i32, _i32, _vp, _i32, ct.c_int, _vp, _vp, _vp],
     "kv_commit_should_stage": [_dbl, _dbl, _u64, _u64, _u64, _u64, ct.c_int],
@@ -487,6 +489,24 @@ def kv_store_gather(layout: KvLayout, d_staging, layers: Sequence, d_block_table
                                  _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
                                  _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
                                  _stream(stream)), "kv_store_gather")
+
+
+def kv_probe_mixed_traffic(layout: KvLayout, d_staging, layers: Sequence, d_block_tables, bt_stride: int,
+                           num_reqs: int, d_jobs, num_jobs: int, d_slots, num_read_slots: int, fill: int,
+                           stream=None) -> None:
+    """Measurement reference for the retrieve (not part of the path): reads every
+    segment of the listed slots and writes `fill` into every destination block of
+    the jobs, interleaved in one launch with no data passing between them.
+    Overwrites those destination blocks."""
+    import torch
+    if len(layers) != layout.num_layers:
+        raise ValueError("one paged tensor per layer is required")
+    _check(lib().kv_probe_mixed_traffic(ct.byref(layout), _dptr(d_staging, None, "staging"), _layer_array(layers),
+                                        _dptr(d_block_tables, torch.int32, "block_tables"), bt_stride, num_reqs,
+                                        _dptr(d_jobs, torch.int32, "jobs") if num_jobs else None, num_jobs,
+                                        _dptr(d_slots, torch.int32, "slots") if num_read_slots else None,
+                                        num_read_slots, int(fill) & 0xFFFFFFFF, _stream(stream)),
+           "kv_probe_mixed_traffic")
 
 
 def _hptr(t, what: str = "host buffer") -> int:

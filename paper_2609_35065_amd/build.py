@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libtempokv.so")
-SOURCES = ["api.hip", "host.cpp", "index_table.cpp", "index.hip", "hash.hip", "copy.hip", "staging.hip", "validate.hip", "controller.cpp"]
+SOURCES = ["api.hip", "host.cpp", "index_table.cpp", "index.hip", "hash.hip", "copy.hip", "staging.hip", "validate.hip", "controller.cpp", "probe.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 instructions.
