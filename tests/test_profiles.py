@@ -111,9 +111,16 @@ def test_ceiling_summary_takes_the_ceiling_launches(tmp_path, monkeypatch):
         for _ in range(n):                          # one reduction per read pass
             i += 1
             out.append({"Dispatch_Id": str(i), "Kernel_Name": red, "Counter_Name": ctr, "Counter_Value": str(reader)})
+        for v in mixed:                             # the independent-mix probe's launches
+            i += 1
+            out.append({"Dispatch_Id": str(i), "Kernel_Name": mix, "Counter_Name": ctr, "Counter_Value": str(v)})
         return out
 
+    mix = ("tkv::(anonymous namespace)::mixed_traffic_kernel(tkv::CopyParams, int const*, int, long, long, "
+           "unsigned int)")
+    mixed = [120, 100, 110]
     _write_csv(str(d / "ceil_fetch" / "c_counter_collection.csv"), rows("FETCH_SIZE", 1000, 10, 100))
+    mixed = [4100, 4100, 4000]
     _write_csv(str(d / "ceil_write" / "c_counter_collection.csv"), rows("WRITE_SIZE", 4000, 4000, 0))
     row = lambda c, v: {"Dispatch_Id": "1", "Kernel_Name": cal, "Counter_Name": c, "Counter_Value": str(v)}
     _write_csv(str(d / "cal_fetch" / "c_counter_collection.csv"), [row("FETCH_SIZE", (4 << 20) / 2)])
@@ -127,6 +134,9 @@ def test_ceiling_summary_takes_the_ceiling_launches(tmp_path, monkeypatch):
     assert float(kv["writes_only_hbm_write_bytes_per_launch"]) == 4000 * 1024
     assert float(kv["unique_read_hbm_read_bytes_per_pass"]) == 100 * 2 * 1024
     assert int(kv["retrieve_launches_in_run"]) == 5 + n
+    assert float(kv["independent_mix_hbm_read_bytes_per_launch"]) == 110 * 2 * 1024     # median, scaled
+    assert float(kv["independent_mix_hbm_write_bytes_per_launch"]) == 4100 * 1024
+    assert bench._label("mixed_traffic_kernel") != "other"
     # no ceiling measured (streaming retrieve, or staged chunks in host memory): no file
     (d / "ceil_fetch.log").write_text('{"config": {"retrieve_variant": "stream"}, "ceiling_launches": %d, '
                                       '"ceiling": null}\n' % n)
