@@ -174,8 +174,8 @@ int kv_index_size(const kv_index *idx, int64_t *out);
 /* Slot of one key on the host view, or -1.  For tests and host policy. */
 int kv_index_find(const kv_index *idx, uint64_t key, int32_t *slot_out);
 
-/* Prefix match (Section 2.1: once a prefix match is known the required
- * objects and their order are known).  For request r with nb_r block hashes
+/* Prefix match (Section 2.1: matching a request's prefix already tells
+ * which objects it will read, and in what order).  For request r with nb_r block hashes
  * and bpc = blocks_per_chunk, chunk j < floor(nb_r/bpc) has key
  * K[r][j] = d_block_hash[d_blk_off[r] + (j+1)*bpc - 1];
  *   d_chunk_slot[d_chunk_off[r] + j] = slot of K[r][j], or -1 if absent
@@ -291,8 +291,8 @@ int kv_group_jobs_by_slot(kv_job *h_jobs, int32_t num_jobs);
 /* ----------------------------------------------------------------------- */
 
 /* The paper separates staging (SSD -> fast tier) from retrieval (fast tier ->
- * GPU), and calls the matched KV stage-ready once every object it needs is
- * present in the fast tier and protected (Section 2.2).  Here pinned host
+ * GPU), and calls the matched KV stage-ready once every object it needs
+ * sits in the fast tier under protection (Section 2.2).  Here pinned host
  * memory stands in for the lower tier and the HBM staging buffer is the fast
  * tier: h_lower_tier holds slots in the same [S][L][2][C][H][D] layout, slot
  * s at byte s*slot_bytes of both buffers.  h_lower_tier should come from
@@ -482,7 +482,7 @@ int kv_ttr_state_aware(int32_t n, const int32_t *h_objs, int32_t num_objects, co
 typedef enum kv_policy {
     KV_POLICY_DEMAND = 0,        /* only when retrieval is requested */
     KV_POLICY_IMMEDIATE = 1,     /* as soon as the claim is reported */
-    KV_POLICY_QUEUE_K = 2,       /* when the request is among the first K waiting */
+    KV_POLICY_QUEUE_K = 2,       /* when at most K-1 waiting requests are ahead of it */
     KV_POLICY_TEMPO_STATIC = 3,  /* TTU <= TTR, TTR = non-resident bytes / static rate, in isolation */
     KV_POLICY_TEMPO = 4          /* TTU <= TTR, TTR from a projection of the staging queue */
 } kv_policy;

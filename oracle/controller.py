@@ -14,9 +14,9 @@ Objects o (staged chunks) of bytes[o].  Fast tier of `capacity` bytes with a
 protected budget `budget` <= capacity.  An object is resident or not, may have
 a staging read outstanding (completion time ready_at[o]), and a protection
 count prot[o] (committed, unreleased claims that need it).  Reserved capacity
-P(t) = sum of bytes[o] over objects with prot[o] > 0: protected objects and
-reservations for outstanding staging, each shared object once (Section 5,
-"Metrics").
+P(t) = sum of bytes[o] over objects with prot[o] > 0: objects held under
+protection, whether resident or still being staged, each shared object
+counted once (Section 5, "Metrics").
 
 Staging device: one FIFO server at `stage_rate` bytes/s (concurrent reads
 share an aggregate rate, Section 3.1); busy_until is when its queue drains.
@@ -46,8 +46,8 @@ unprotected resident objects (ties by id) until it fits; an unprotected object
 that cannot fit is not retained.
 
 Policies (Section 5 "Policies"): DEMAND (eligible only when retrieval is
-requested), IMMEDIATE (when reported), QUEUE_K (when among the first K
-waiting), TEMPO_STATIC (TTU <= TTR with TTR = non-resident bytes /
+requested), IMMEDIATE (when reported), QUEUE_K (when at most K-1 waiting
+requests are ahead of it), TEMPO_STATIC (TTU <= TTR with TTR = non-resident bytes /
 static_rate, in isolation), TEMPO (TTU <= TTR with TTR from a projection of
 the staging queue: already-queued objects keep their completion times, new
 reads are appended in manifest order; the last object decides, Section 3.1).

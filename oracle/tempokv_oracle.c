@@ -9,15 +9,16 @@
  *
  * What the paper fixes and what it leaves open
  * --------------------------------------------
- * TempoKV (Section 4, "Runtime and controller integration") reuses LMCache's
- * prefix lookup and GPU-transfer paths unchanged and does not describe them.
+ * TempoKV (Section 4, "Runtime and controller integration") takes the prefix
+ * matching and the fast-tier-to-GPU copy from LMCache as they are and does
+ * not describe them.
  * The data-parallel path computed here is therefore defined as follows; each
  * function names the passage it follows and the reading taken where the
  * paper is silent.
  *
- *   - A KV object is an independently identified unit of reusable prefix KV,
- *     read-only during reuse; once a prefix match is known the required
- *     objects and their order are known (Section 2.1).  Here one object is one
+ *   - Reusable prefix KV is handled as separately named objects that are
+ *     only read while reused, and matching a request's prefix already tells
+ *     which objects it needs and in what order (Section 2.1).  Here one object is one
  *     LMCache chunk of C tokens; only complete chunks are retained and the
  *     final incomplete chunk stays uncached (Section 5, "Workload").
  *   - Objects are identified by a chained 64-bit hash over 16-token blocks

@@ -1,14 +1,15 @@
 """Pins for the commitment decision, case by case from Section 3.2.
 
-  * "eligible when the estimated laxity TTU - TTR is <= 0 or the runtime
-    requests retrieval" (timing-based eligibility);
+  * timing-based eligibility: a claim may commit once its estimated laxity
+    TTU - TTR has reached zero or gone below it, or as soon as retrieval of
+    its KV is requested;
   * positive laxity predicts early readiness: not eligible, decision deferred;
   * a protected commitment needs the claim's full footprint within the
-    protected-capacity budget; only bytes not already covered by another
-    commitment are newly reserved ("Shared staging and resource lifecycle");
+    protected-capacity budget; bytes that an earlier commitment already
+    protects are not reserved again ("Shared staging and resource lifecycle");
   * without sufficient capacity the claim stays PLANNED (here BLOCKED);
-  * a claim that cannot obtain protection when retrieval is requested takes
-    the ordinary retrieval path, exclusive of commitment (ORDINARY).
+  * a claim whose retrieval is requested but which cannot be protected is
+    read through the ordinary retrieval path instead, uncommitted (ORDINARY).
 """
 import itertools
 import math

@@ -3,8 +3,8 @@
 Lookup is checked against a brute-force prefix match on tokens that uses no
 hashing at all: chunk j of request r is a hit iff some stored chunk's full
 token prefix equals the request's first (j+1)*C tokens, and the hit count is
-the longest such run from chunk 0 (prefix semantics: once a prefix match is
-known, the required objects and their order are known, Section 2.1).
+the longest such run from chunk 0 (prefix semantics: the matched prefix
+fixes which objects a request reads and in what order, Section 2.1).
 
 Job build is checked against its invariants: retrieve jobs are exactly the
 hit prefix; every distinct missing key gets at most one store job, the first

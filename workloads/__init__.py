@@ -604,8 +604,8 @@ class StagingScenario:
 
 def policy_scenario(ratio: float, seed: int = 7, kv_bytes_per_token: int = 128 * 1024, chunk: int = 256,
                     gap_s: float = 0.5, out_tokens: int = 128, question_tokens: int = 32) -> StagingScenario:
-    """Shaped like the paper's policy experiment (Section 5): 12 documents, four
-    from each of three length groups spanning 16,078-67,744 tokens (lengths
+    """Shaped like the paper's policy experiment (Section 5): 12 documents in
+    three length groups of 4, together spanning 16,078-67,744 tokens (lengths
     drawn uniformly inside each group, no dataset text), one request per
     document in a fixed random order every ``gap_s`` seconds; the prefix
     ``ratio`` of each document is retained as complete 256-token chunks (each
