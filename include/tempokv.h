@@ -383,7 +383,7 @@ typedef enum kv_commit_decision {
  * ttu_s <= ttr_s, so infinite estimates behave) or retrieval_requested.  A
  * commitment needs the claim's full footprint within the protected budget
  * (claim_total_bytes <= budget_bytes) and its newly reserved bytes -- those
- * not already covered by another commitment -- within the free protected
+ * that no earlier commitment protects yet -- within the free protected
  * capacity (claim_new_bytes <= free_protected_bytes).  Returns a
  * kv_commit_decision, or KV_EINVAL for a NaN estimate or claim_new_bytes >
  * claim_total_bytes.  Aging TTU by elapsed time is the caller's job. */

@@ -477,7 +477,7 @@ enum { OR_DEFER = 0, OR_COMMIT = 1, OR_BLOCKED = 2, OR_ORDINARY = 3, OR_EINVAL =
 /* Eligibility: laxity TTU - TTR <= 0, evaluated as TTU <= TTR so that it also
  * holds for infinite estimates, or retrieval requested.  Capacity: the whole
  * claim footprint must fit the protected budget, and the bytes the claim
- * newly reserves (those not already covered by another commitment) must fit
+ * newly reserves (those no earlier commitment protects yet) must fit
  * the free protected capacity.  An eligible claim that does not fit stays
  * PLANNED (BLOCKED) unless retrieval was requested, in which case it takes
  * the ordinary retrieval path (ORDINARY). */

@@ -10,7 +10,7 @@
 // FCFS order (Section 3.2 "Commitment and replanning") -- and asks the
 // commitment rule kv_commit_should_stage for each: eligibility from the
 // policy (or the retrieval request), capacity from the protected budget.  A
-// blocked claim does not block the others; a commitment is never revoked; a
+// claim that cannot commit holds up no later claim; a commitment is never revoked; a
 // claim that cannot be protected when its retrieval is requested takes the
 // ordinary path (Section 3.2 "Protected capacity and on-demand retrieval").
 //

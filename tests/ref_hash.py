@@ -1,7 +1,7 @@
 """A second, independent implementation of the library's chained prefix hash.
 
 Written in plain Python integers from the documented definition of
-``kv_hash_prefix`` (the paper reuses LMCache's prefix lookup without defining
+``kv_hash_prefix`` (the paper takes its prefix matching from LMCache without defining
 a hash, Section 4, so the definition is this library's own):
 
     M      SplitMix64's output finalizer: xor-shift right 30, multiply by

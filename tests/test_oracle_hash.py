@@ -1,6 +1,6 @@
 """Pins for the oracle's chained prefix hash.
 
-The paper does not define the hash (it reuses LMCache's prefix lookup,
+The paper does not define the hash (it takes its prefix matching from LMCache,
 Section 4), so the oracle's hash is this library's own definition: a 64-bit
 chain over 16-token blocks built on the SplitMix64 finalizer M.  These tests
 pin it to things outside the oracle:
