@@ -297,6 +297,24 @@ def test_retrieve_as_rejects_unknown_kinds():
                                         None) == kv.KV_EINVAL
 
 
+def test_probe_checks_arguments_before_any_launch():
+    # the measurement reference takes the retrieve's arguments plus the slots it reads
+    lo = _layout()
+    L = kv.lib()
+    f = L.kv_probe_mixed_traffic
+    good = (ct.c_void_p * 2)(0x10000, 0x20000)
+    A, J, S = 0x10000, 0x20000, 0x30000                  # block tables, jobs, slots (never dereferenced)
+    assert f(ct.byref(_layout(num_layers=0)), A, good, A, 10, 2, J, 1, S, 1, 7, None) == kv.KV_EINVAL
+    assert f(ct.byref(lo), 0x10008, good, A, 10, 2, J, 1, S, 1, 7, None) == kv.KV_EALIGN
+    assert f(ct.byref(lo), A, good, A, 10, 2, None, 1, S, 1, 7, None) == kv.KV_EINVAL
+    assert f(ct.byref(lo), A, good, A, 10, 2, J, 1, S, -1, 7, None) == kv.KV_EINVAL
+    assert f(ct.byref(lo), A, good, A, 10, 2, J, 1, None, 1, 7, None) == kv.KV_EINVAL
+    # 2^31 or more segments in one launch: refused (keeps the kernel's index arithmetic in 64 bits)
+    assert f(ct.byref(lo), A, good, A, 10, 2, J, 2**31 - 1, S, 0, 7, None) == kv.KV_EINVAL
+    # nothing to move: valid, enqueues nothing
+    assert f(ct.byref(lo), A, good, A, 10, 2, None, 0, None, 0, 7, None) == kv.KV_OK
+
+
 @pytest.mark.parametrize("seed", range(10))
 def test_chunk_keys_match_oracle(seed):
     bh, blk_off, chunk_off, bpc, cs, hit = _lookup_case(seed)
